@@ -1,0 +1,115 @@
+// Device helpers shared by the SelKV kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace selkv {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 storage is kept as raw 16-bit patterns.
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 (NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+// A 16-byte chunk of a row in storage type T, as raw 32-bit words.
+struct Chunk16 {
+  uint32_t w[4];
+};
+
+__device__ __forceinline__ Chunk16 load16(const void* p) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  Chunk16 c;
+  c.w[0] = v.x; c.w[1] = v.y; c.w[2] = v.z; c.w[3] = v.w;
+  return c;
+}
+
+__device__ __forceinline__ void store16(void* p, const Chunk16& c) {
+  *reinterpret_cast<uint4*>(p) = make_uint4(c.w[0], c.w[1], c.w[2], c.w[3]);
+}
+
+__device__ __forceinline__ Chunk16 zero16() {
+  Chunk16 c;
+  c.w[0] = c.w[1] = c.w[2] = c.w[3] = 0u;
+  return c;
+}
+
+// Elements per 16-byte chunk and their conversion to fp32.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int kPerChunk = 4;
+  __device__ static __forceinline__ float get(const Chunk16& c, int e) { return __uint_as_float(c.w[e]); }
+  __device__ static __forceinline__ void put(Chunk16& c, int e, float x) { c.w[e] = __float_as_uint(x); }
+};
+template <> struct Elem<bf16_t> {
+  static constexpr int kPerChunk = 8;
+  __device__ static __forceinline__ float get(const Chunk16& c, int e) {
+    const uint32_t w = c.w[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  __device__ static __forceinline__ void put(Chunk16& c, int e, float x) {
+    const uint32_t h = f32_to_bf16(x);
+    uint32_t& w = c.w[e >> 1];
+    w = (e & 1) ? ((w & 0x0000ffffu) | (h << 16)) : ((w & 0xffff0000u) | h);
+  }
+};
+
+// One 16x16 fp32 tile update D += A * B from 16-byte chunks holding the
+// lane's A and B fragments (16x16x32 bf16 MFMA, or four 16x16x4 fp32 MFMAs).
+template <typename T> struct Mma;
+template <> struct Mma<bf16_t> {
+  __device__ static __forceinline__ f32x4 step(const Chunk16& a, const Chunk16& b, f32x4 acc) {
+    const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+    const bf16x8 bv = __builtin_bit_cast(bf16x8, b);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+  }
+};
+template <> struct Mma<float> {
+  __device__ static __forceinline__ f32x4 step(const Chunk16& a, const Chunk16& b, f32x4 acc) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), acc, 0, 0, 0);
+    return acc;
+  }
+};
+
+__device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, 64); }
+__device__ __forceinline__ int xor_shfl(int v, int mask) { return __shfl_xor(v, mask, 64); }
+
+// Sum over the 16 lanes of a lane group (lanes 16q .. 16q+15), same result on all of them.
+__device__ __forceinline__ float sum16(float v) {
+  v += xor_shfl(v, 1);
+  v += xor_shfl(v, 2);
+  v += xor_shfl(v, 4);
+  v += xor_shfl(v, 8);
+  return v;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(v, off, 64);
+    if (lane >= off) v += u;
+  }
+  return v;
+}
+
+}  // namespace selkv

@@ -1,0 +1,58 @@
+// Host-side launch plans and kernel launchers (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "selkv.h"
+
+namespace selkv {
+
+// Validated, derived sizes of one problem.
+struct Shape {
+  int64_t heads;     // batch * n_heads_kv
+  int n, d, G, W, R; // R = G * W window rows per KV head
+  int m, mr, ms;     // budget of Sec. 3.1
+  int n_cand;        // n - mr
+  int nb;            // number of routing buckets
+};
+
+// Score pass layout: key chunks per KV head and row groups.
+struct ScorePlan {
+  int chunk_keys;    // keys per workgroup (multiple of 64)
+  int nchunks;       // chunks per KV head
+  int rows_per_group;  // rows held in registers by one pass (16 * row blocks)
+  int nrg;           // row groups
+  int rpad;          // nrg * rows_per_group
+  size_t part_off, stats_off, c_off, bytes;
+};
+
+struct DecodePlan {
+  int chunk;         // keys per workgroup (multiple of 128)
+  int nsplit;        // workgroups per KV head
+  size_t bytes;
+};
+
+ScorePlan plan_score(const Shape& s, int dtype);
+DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G);
+size_t bucket_offsets_bytes(const Shape& s);
+
+// Launchers return hipSuccess or the launch error.
+hipError_t launch_score(const Shape& s, const ScorePlan& plan, int dtype, float scale, const void* K,
+                        const void* V, const void* Qwin, float* score, float* attn, float* vnorm,
+                        int pool_kernel, void* ws, hipStream_t st);
+hipError_t launch_select(const Shape& s, const float* score, int32_t* kept, int32_t* evicted, hipStream_t st);
+hipError_t launch_bucket_offsets(const Shape& s, int bucket, const int32_t* kept, int32_t* offs, hipStream_t st);
+hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
+                               const void* K, const void* V, const float* attn, const float* vnorm,
+                               const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
+                               void* V_out, int32_t* target, float* gate, hipStream_t st);
+hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
+                              const int32_t* evicted, const int32_t* offs, const int32_t* target,
+                              const float* gate, float* bias, hipStream_t st);
+hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int d, int G, int dtype, float scale,
+                         const DecodePlan& plan, const void* q, const void* K, const void* V, const float* bias,
+                         float* out, void* ws, hipStream_t st);
+
+}  // namespace selkv

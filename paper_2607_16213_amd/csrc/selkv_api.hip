@@ -1,0 +1,236 @@
+// C ABI of libselkv: argument validation, workspace sizing, dispatch.
+// Every check happens on the host before anything is launched.
+#include <math.h>
+#include <string.h>
+
+#include "internal.hpp"
+#include "selkv.h"
+
+using namespace selkv;
+
+namespace {
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Validates the fields every compression call uses and derives the sizes.
+selkv_status make_shape(const selkv_params* p, Shape* s) {
+  if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
+  if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
+  if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || p->seq_len < 1) return SELKV_EINVAL;
+  if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+  if (p->window < 1 || p->window > p->seq_len) return SELKV_EINVAL;
+  if (p->pool_kernel < 1 || (p->pool_kernel % 2) == 0) return SELKV_EINVAL;
+  if (p->recent < 0) return SELKV_EINVAL;
+  if (p->bucket < 1) return SELKV_EINVAL;
+  if (p->bucket > 64) return SELKV_EUNSUPPORTED;
+  if (!(p->budget_ratio > 0.0 && p->budget_ratio <= 1.0)) return SELKV_EINVAL;
+  if (!(p->scale >= 0.f) || !isfinite(p->scale)) return SELKV_EINVAL;
+  if (!isfinite(p->alpha)) return SELKV_EINVAL;
+  if (!(p->gate_temperature > 0.f) || !isfinite(p->gate_temperature) || !isfinite(p->gate_threshold))
+    return SELKV_EINVAL;
+  if (p->gate_mode < SELKV_GATE_COSINE || p->gate_mode > SELKV_GATE_MERGE_ALL) return SELKV_EINVAL;
+  if (p->route_mode != SELKV_ROUTE_BUCKET && p->route_mode != SELKV_ROUTE_FULL_COSINE) return SELKV_EINVAL;
+  const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
+  if (heads > 65535) return SELKV_EUNSUPPORTED;              // grid y dimension
+  const int64_t R = (int64_t)p->group * p->window;
+  if (R > 4096) return SELKV_EUNSUPPORTED;
+  const double md = floor(p->budget_ratio * (double)p->seq_len);
+  const int m = (int)md;
+  if (m < 1) return SELKV_EINVAL;
+  s->heads = heads;
+  s->n = p->seq_len;
+  s->d = p->head_dim;
+  s->G = p->group;
+  s->W = p->window;
+  s->R = (int)R;
+  s->m = m;
+  s->mr = p->recent < m ? p->recent : m;
+  s->ms = m - s->mr;
+  s->n_cand = s->n - s->mr;
+  s->nb = (s->n + p->bucket - 1) / p->bucket;
+  return SELKV_OK;
+}
+
+float eff_scale(const selkv_params* p) { return p->scale > 0.f ? p->scale : 1.f / sqrtf((float)p->head_dim); }
+
+size_t elem_size(const selkv_params* p) { return p->kv_dtype == SELKV_BF16 ? 2 : 4; }
+
+selkv_status hip_status(hipError_t e) { return e == hipSuccess ? SELKV_OK : SELKV_EHIP; }
+
+selkv_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return SELKV_OK;
+  if (!ws || ws_bytes < need) return SELKV_EWORKSPACE;
+  if (!aligned(ws, 256)) return SELKV_EALIGN;
+  return SELKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+SELKV_API void selkv_params_init(selkv_params* p) {
+  if (!p) return;
+  memset(p, 0, sizeof(*p));
+  p->struct_size = sizeof(selkv_params);
+  p->batch = 1;
+  p->n_heads_kv = 8;
+  p->group = 4;
+  p->head_dim = 128;
+  p->seq_len = 0;
+  p->window = 32;
+  p->pool_kernel = 5;
+  p->recent = 16;
+  p->bucket = 32;
+  p->kv_dtype = SELKV_BF16;
+  p->gate_mode = SELKV_GATE_COSINE;
+  p->route_mode = SELKV_ROUTE_BUCKET;
+  p->scale = 0.f;
+  p->alpha = 0.5f;
+  p->gate_threshold = 0.f;
+  p->gate_temperature = 1.f;
+  p->budget_ratio = 0.25;
+}
+
+SELKV_API selkv_status selkv_budget(const selkv_params* p, int32_t* m, int32_t* m_recent, int32_t* m_select) {
+  Shape s;
+  const selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (m) *m = s.m;
+  if (m_recent) *m_recent = s.mr;
+  if (m_select) *m_select = s.ms;
+  return SELKV_OK;
+}
+
+SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call, int32_t cache_len, size_t* bytes) {
+  if (!bytes) return SELKV_EINVAL;
+  if (call == SELKV_CALL_DECODE) {
+    if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
+    if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || p->group > 8 || cache_len < 1) return SELKV_EINVAL;
+    if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+    *bytes = plan_decode((int64_t)p->batch * p->n_heads_kv, cache_len, p->head_dim, p->group).bytes;
+    return SELKV_OK;
+  }
+  Shape s;
+  const selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  switch (call) {
+    case SELKV_CALL_SCORE: *bytes = plan_score(s, p->kv_dtype).bytes; return SELKV_OK;
+    case SELKV_CALL_SELECT: *bytes = 0; return SELKV_OK;
+    case SELKV_CALL_MERGE:
+    case SELKV_CALL_BIAS: *bytes = bucket_offsets_bytes(s); return SELKV_OK;
+    default: return SELKV_EINVAL;
+  }
+}
+
+SELKV_API selkv_status selkv_score(const selkv_params* p, const void* K, const void* V, const void* Qwin,
+                                   float* score, float* attn, float* vnorm, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (!K || !V || !Qwin || !score || !attn || !vnorm) return SELKV_EINVAL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Qwin, 16) || !aligned(score, 4) || !aligned(attn, 4) ||
+      !aligned(vnorm, 4))
+    return SELKV_EALIGN;
+  const ScorePlan plan = plan_score(s, p->kv_dtype);
+  if ((st = check_ws(ws, ws_bytes, plan.bytes)) != SELKV_OK) return st;
+  return hip_status(launch_score(s, plan, p->kv_dtype, eff_scale(p), K, V, Qwin, score, attn, vnorm,
+                                 p->pool_kernel, ws, stream));
+}
+
+SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, int32_t* kept_idx,
+                                    int32_t* evicted_idx, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (!score || !kept_idx || (!evicted_idx && s.n > s.m)) return SELKV_EINVAL;
+  if (!aligned(score, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4)) return SELKV_EALIGN;
+  return hip_status(launch_select(s, score, kept_idx, evicted_idx, stream));
+}
+
+SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const void* V, const float* attn,
+                                   const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx,
+                                   void* K_out, void* V_out, int32_t* target, float* gate, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (p->route_mode != SELKV_ROUTE_BUCKET) return SELKV_EUNSUPPORTED;
+  const bool has_ev = s.n > s.m;
+  if (!K || !V || !attn || !vnorm || !kept_idx || !K_out || !V_out) return SELKV_EINVAL;
+  if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(K_out, 16) || !aligned(V_out, 16) || !aligned(attn, 4) ||
+      !aligned(vnorm, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
+      !aligned(gate, 4))
+    return SELKV_EALIGN;
+  const size_t need = bucket_offsets_bytes(s);
+  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
+  int32_t* offs = static_cast<int32_t*>(ws);
+  hipError_t e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  e = launch_merge_bucket(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold, p->gate_temperature, K, V,
+                          attn, vnorm, kept_idx, evicted_idx, offs, K_out, V_out, target, gate, stream);
+  return hip_status(e);
+}
+
+SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,
+                                  const int32_t* evicted_idx, const int32_t* target, const float* gate,
+                                  float* bias, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (p->route_mode != SELKV_ROUTE_BUCKET) return SELKV_EUNSUPPORTED;
+  const bool has_ev = s.n > s.m;
+  if (!attn || !kept_idx || !bias) return SELKV_EINVAL;
+  if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
+  if (!aligned(attn, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
+      !aligned(gate, 4) || !aligned(bias, 4))
+    return SELKV_EALIGN;
+  const size_t need = bucket_offsets_bytes(s);
+  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
+  int32_t* offs = static_cast<int32_t*>(ws);
+  hipError_t e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  e = launch_bias_bucket(s, p->bucket, p->alpha, attn, kept_idx, evicted_idx, offs, target, gate, bias, stream);
+  return hip_status(e);
+}
+
+SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
+                                         const float* bias, int32_t cache_len, float* out, void* ws,
+                                         size_t ws_bytes, hipStream_t stream) {
+  if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
+  if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
+  if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || cache_len < 1) return SELKV_EINVAL;
+  if (p->group > 8) return SELKV_EUNSUPPORTED;
+  if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+  if (!(p->scale >= 0.f) || !isfinite(p->scale)) return SELKV_EINVAL;
+  const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
+  if (heads > 65535) return SELKV_EUNSUPPORTED;
+  if (!q || !K || !V || !out) return SELKV_EINVAL;
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(bias, 4) || !aligned(out, 4))
+    return SELKV_EALIGN;
+  const DecodePlan plan = plan_decode(heads, cache_len, p->head_dim, p->group);
+  selkv_status st = check_ws(ws, ws_bytes, plan.bytes);
+  if (st != SELKV_OK) return st;
+  return hip_status(launch_decode(heads, p->n_heads_kv, cache_len, p->head_dim, p->group, p->kv_dtype,
+                                  eff_scale(p), plan, q, K, V, bias, out, ws, stream));
+}
+
+SELKV_API const char* selkv_status_string(selkv_status s) {
+  switch (s) {
+    case SELKV_OK: return "success";
+    case SELKV_EINVAL: return "invalid argument";
+    case SELKV_EDTYPE: return "unknown kv dtype";
+    case SELKV_EUNSUPPORTED: return "unsupported configuration";
+    case SELKV_EALIGN: return "misaligned pointer";
+    case SELKV_EWORKSPACE: return "workspace missing or too small";
+    case SELKV_EHIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+SELKV_API int32_t selkv_abi_version(void) { return SELKV_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+"""The C ABI library on the host: it loads, exports every symbol declared in
+include/selkv.h, its struct layout matches the binding, and its host-only
+logic (budget, workspace sizing, argument validation) behaves as documented.
+No call here reaches a kernel launch."""
+import ctypes
+import json
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "selkv.h")
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_16213_amd import selkv
+    return selkv
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"SELKV_API\s+[\w\s\*]+?\b(selkv_\w+)\s*\(", text)
+
+
+def test_header_symbols_exported(S):
+    names = declared_functions()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(S.lib, name), name
+    dyn = subprocess.run(["nm", "-D", "--defined-only", S.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(line.split()[-1] for line in dyn.splitlines() if line.strip())
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+
+
+def test_struct_layout_matches_c(S):
+    fields = [f for f, _ in S.Params._fields_]
+    src = ["#include <stdio.h>", "#include <stddef.h>", '#include "selkv.h"', "int main(void){",
+           'printf("{\\"size\\": %zu", sizeof(selkv_params));']
+    for f in fields:
+        src.append(f'printf(", \\"{f}\\": %zu", offsetof(selkv_params, {f}));')
+    src.append('printf("}\\n"); return 0; }')
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "layout.c")
+        open(c, "w").write("\n".join(src))
+        exe = os.path.join(d, "layout")
+        r = subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", f"-I{ROOT}/include", "-I/opt/rocm/include", c, "-o", exe],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+        layout = json.loads(subprocess.run([exe], capture_output=True, text=True).stdout)
+    assert layout["size"] == ctypes.sizeof(S.Params)
+    for f in fields:
+        assert layout[f] == getattr(S.Params, f).offset, f
+
+
+def test_params_init_defaults(S):
+    p = S.params()
+    assert p.struct_size == ctypes.sizeof(S.Params)
+    assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
+    assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
+    assert S.lib.selkv_abi_version() == 1
+    assert S.lib.selkv_status_string(0) == b"success"
+
+
+def test_budget_matches_golden(S):
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_worked.json")))["budget_cases"]["cases"]
+    for n, rho, m, ms in gold:
+        p = S.params(seq_len=n, budget_ratio=rho, window=min(32, n))
+        got = S.budget(p)
+        assert got[0] == m and got[2] == ms, (n, rho, got)
+
+
+def test_workspace_sizes(S):
+    p = S.params(seq_len=8192)
+    assert S.workspace_bytes(p, S.CALL_SCORE) > 8 * 8192 * 4
+    assert S.workspace_bytes(p, S.CALL_SELECT) == 0
+    assert S.workspace_bytes(p, S.CALL_MERGE) >= 8 * (8192 // 32 + 1) * 4
+    assert S.workspace_bytes(p, S.CALL_DECODE, 2048) > 0
+
+
+def test_validation_codes(S):
+    def st(p, call=S.CALL_SCORE):
+        b = ctypes.c_size_t()
+        return S.lib.selkv_workspace_size(ctypes.byref(p), call, 16, ctypes.byref(b))
+    assert st(S.params(seq_len=100)) == 0
+    assert st(S.params(seq_len=100, head_dim=96)) == 3          # EUNSUPPORTED
+    assert st(S.params(seq_len=100, kv_dtype=7)) == 2           # EDTYPE
+    assert st(S.params(seq_len=100, window=101)) == 1           # W > n
+    assert st(S.params(seq_len=100, pool_kernel=4)) == 1        # even K
+    assert st(S.params(seq_len=100, budget_ratio=0.0)) == 1
+    assert st(S.params(seq_len=100, budget_ratio=1.5)) == 1
+    assert st(S.params(seq_len=3, window=3, budget_ratio=0.25)) == 1   # m = 0
+    assert st(S.params(seq_len=100, gate_temperature=0.0)) == 1
+    assert st(S.params(seq_len=100, bucket=65)) == 3
+    assert st(S.params(seq_len=100, group=9), S.CALL_DECODE) == 1
+    p = S.params(seq_len=100)
+    p.struct_size = 4
+    assert st(p) == 1
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_call_validation_before_launch(S):
+    """Invalid calls return a status before any launch (fake pointers never
+    get dereferenced: a launch here would fail with EHIP instead)."""
+    p = S.params(seq_len=256)
+    fake = ctypes.c_void_p(0x10000)
+    mis = ctypes.c_void_p(0x10002)
+    null = None
+    f = S.lib.selkv_score
+    assert f(ctypes.byref(p), null, fake, fake, fake, fake, fake, fake, 1 << 30, None) == 1
+    assert f(ctypes.byref(p), mis, fake, fake, fake, fake, fake, fake, 1 << 30, None) == 4
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, null, 0, None) == 5
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, fake, 16, None) == 5
+    g = S.lib.selkv_decode_attn
+    assert g(ctypes.byref(p), fake, fake, fake, null, 0, fake, fake, 1 << 30, None) == 1      # cache_len 0
+    assert g(ctypes.byref(p), fake, fake, fake, ctypes.c_void_p(0x10001), 64, fake, fake, 1 << 30, None) == 4
+    pf = S.params(seq_len=256, route_mode="full_cosine")
+    m = S.lib.selkv_merge
+    assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, 1 << 30, None) == 3

@@ -1,0 +1,374 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded, storage-rounded inputs.
+
+Stage-wise checks feed every GPU call the oracle's own inputs for that step
+(so a selection near-tie cannot cascade); end-to-end checks run the whole
+GPU pipeline and allow only selection swaps between near-tied scores.
+Bars: indices and gathered keys bit-exact; score / attn / vnorm within 1e-4
+relative (fp32 arithmetic on exact inputs); merged values, decode outputs and
+gates within 1e-4 (fp32 storage) or 2e-2 (bf16 storage); bias within
+alpha * that tolerance.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import selkv_oracle as O
+from paper_2607_16213_amd import synth
+from tests.parity_util import (SCORE_RTOL, TOL, assert_close_elem, assert_close_rows, compare_end_to_end, dtype_name,
+                               np64, oracle_head_score, oracle_scale)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2607_16213_amd import selkv
+    return selkv
+
+
+def to_dev(x, dtype):
+    return torch.as_tensor(np.ascontiguousarray(x)).to(dtype).to(DEV).contiguous()
+
+
+def make_params(S, w_or_case, **kw):
+    base = dict(batch=w_or_case["batch"], n_heads_kv=w_or_case["H"], group=w_or_case["G"],
+                head_dim=w_or_case["d"], seq_len=w_or_case["n"], window=w_or_case["W"],
+                kv_dtype=w_or_case["dtype"])
+    base.update(kw)
+    return S.params(**base)
+
+
+def case_from_workload(w: synth.Workload, **over):
+    return dict(batch=w.batch, H=w.n_heads_kv, G=w.group, d=w.head_dim, n=w.seq_len, W=w.window,
+                dtype=w.dtype, **over)
+
+
+def oracle_chain(K64, V64, Q64, p, gate_mode):
+    """The oracle's steps for one head, chaining fp32-rounded values between
+    steps exactly as they are handed to the GPU stage calls."""
+    n = K64.shape[0]
+    m, mr, ms = O.budget(n, p.budget_ratio, p.recent)
+    a, vn, s = oracle_head_score(K64, V64, Q64, p)
+    s32 = s.astype(np.float32).astype(np.float64)
+    kept, ev = O.select(s32, n, m, mr)
+    a32 = a.astype(np.float32).astype(np.float64)
+    target = O.route_bucket(a32, kept, ev, p.bucket)
+    g = O.gate(V64, kept, ev, target, gate_mode, float(np.float32(p.gate_threshold)),
+               float(np.float32(p.gate_temperature)))
+    k_out, v_out, _ = O.merge(K64, V64, a32, kept, ev, target, g)
+    g32 = g.astype(np.float32).astype(np.float64)
+    bias = O.ratio_bias(a32, kept, ev, target, g32, float(np.float32(p.alpha)))
+    return dict(a=a, vn=vn, s=s, s32=s32, a32=a32, kept=kept, ev=ev, target=target, g=g, g32=g32,
+                k_out=k_out, v_out=v_out, bias=bias, m=m, mr=mr, ms=ms)
+
+
+GATE = {0: "cosine", 1: "drop", 2: "merge_all"}
+
+
+def gpu_head(comp, b, h):
+    """One (batch, head) slice of the GPU outputs as float64 / int numpy."""
+    return dict(attn=np64(comp.attn[b, h]), score=np64(comp.score[b, h]), kept=comp.kept[b, h].cpu().numpy(),
+                evicted=comp.evicted[b, h].cpu().numpy(), target=comp.target[b, h].cpu().numpy(),
+                gate=np64(comp.gate[b, h]), v_out=np64(comp.V_out[b, h]), bias=np64(comp.bias[b, h]),
+                K_out=np64(comp.K_out[b, h]))
+
+
+def run_stagewise(S, p, K, V, Qwin, heads=None):
+    """All five calls checked stage by stage; returns the oracle chains."""
+    B, H, n, d = K.shape
+    tol = TOL[dtype_name(K)]
+    m, mr, ms = S.budget(p)
+    comp = S.Compressor(p, DEV)
+    # ---- score (raw inputs)
+    S.score(p, K, V, Qwin, comp.score, comp.attn, comp.vnorm, comp.ws_score)
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(K), np64(V), np64(Qwin)
+    G = p.group
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    chains = {}
+    for (b, h) in heads:
+        ch = oracle_chain(K64[b, h], V64[b, h], Q64[b, h * G:(h + 1) * G], p, GATE[p.gate_mode])
+        chains[(b, h)] = ch
+        assert_close_elem(np64(comp.attn[b, h]), ch["a"], SCORE_RTOL, f"attn[{b},{h}]")
+        assert_close_elem(np64(comp.vnorm[b, h]), ch["vn"], SCORE_RTOL, f"vnorm[{b},{h}]")
+        assert_close_elem(np64(comp.score[b, h]), ch["s"], SCORE_RTOL, f"score[{b},{h}]")
+    # ---- select, fed the oracle's fp32 scores (heads not sampled keep GPU scores)
+    s_in = comp.score.clone()
+    for (b, h), ch in chains.items():
+        s_in[b, h] = torch.as_tensor(ch["s32"], dtype=torch.float32)
+    S.select(p, s_in, comp.kept, comp.evicted)
+    torch.cuda.synchronize()
+    for (b, h), ch in chains.items():
+        np.testing.assert_array_equal(comp.kept[b, h].cpu().numpy(), ch["kept"], err_msg=f"kept[{b},{h}]")
+        np.testing.assert_array_equal(comp.evicted[b, h].cpu().numpy(), ch["ev"], err_msg=f"evicted[{b},{h}]")
+    # ---- merge, fed oracle attn / vnorm / kept / evicted
+    a_in, vn_in = comp.attn.clone(), comp.vnorm.clone()
+    kept_in, ev_in = comp.kept.clone(), comp.evicted.clone()
+    for (b, h), ch in chains.items():
+        a_in[b, h] = torch.as_tensor(ch["a32"], dtype=torch.float32)
+        vn_in[b, h] = torch.as_tensor(ch["vn"], dtype=torch.float32)
+        kept_in[b, h] = torch.as_tensor(ch["kept"], dtype=torch.int32)
+        ev_in[b, h] = torch.as_tensor(ch["ev"], dtype=torch.int32)
+    S.merge(p, K, V, a_in, vn_in, kept_in, ev_in, comp.K_out, comp.V_out, comp.target, comp.gate, comp.ws_merge)
+    torch.cuda.synchronize()
+    for (b, h), ch in chains.items():
+        np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), ch["target"], err_msg=f"target[{b},{h}]")
+        assert np.abs(np64(comp.gate[b, h]) - ch["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(ch["kept"])]), f"K_out[{b},{h}]"
+        assert_close_rows(np64(comp.V_out[b, h]), ch["v_out"], tol, f"V_out[{b},{h}]")
+    # ---- bias, fed oracle target / gate
+    t_in, g_in = comp.target.clone(), comp.gate.clone()
+    for (b, h), ch in chains.items():
+        t_in[b, h] = torch.as_tensor(ch["target"], dtype=torch.int32)
+        g_in[b, h] = torch.as_tensor(ch["g32"], dtype=torch.float32)
+    S.bias(p, a_in, kept_in, ev_in, t_in, g_in, comp.bias, comp.ws_bias)
+    torch.cuda.synchronize()
+    alpha = float(np.float32(p.alpha))
+    for (b, h), ch in chains.items():
+        err = np.abs(np64(comp.bias[b, h]) - ch["bias"]).max(initial=0)
+        assert err <= max(abs(alpha), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
+        unabsorbed = np.setdiff1d(np.arange(m), ch["target"][ch["g32"] * ch["a32"][ch["ev"]] > 0])
+        assert (comp.bias[b, h].cpu().numpy()[unabsorbed] == 0).all(), "bias must be exactly 0 where R = 1"
+    return comp, chains
+
+
+def run_decode_check(S, p, chains, K, steps=3, seed=0):
+    """Decode over the oracle's compressed caches (values rounded to storage)."""
+    B, H = p.batch, p.n_heads_kv
+    G, d, dt = p.group, p.head_dim, K.dtype
+    tol = TOL[dtype_name(K)]
+    m = next(iter(chains.values()))["m"]
+    kc = torch.zeros((B, H, m, d), dtype=dt)
+    vc = torch.zeros((B, H, m, d), dtype=dt)
+    bias = torch.zeros((B, H, m), dtype=torch.float32)
+    for (b, h), ch in chains.items():
+        kc[b, h] = torch.as_tensor(ch["k_out"]).to(dt)
+        vc[b, h] = torch.as_tensor(ch["v_out"]).to(dt)
+        bias[b, h] = torch.as_tensor(ch["bias"]).to(torch.float32)
+    kc_d, vc_d, bias_d = kc.to(DEV), vc.to(DEV), bias.to(DEV)
+    dec = S.Decoder(p, m, DEV)
+    g = torch.Generator().manual_seed(1234 + seed)
+    for step in range(steps):
+        q = torch.randn((B, H * G, d), generator=g).to(dt)
+        out = dec.run(q.to(DEV), kc_d, vc_d, bias_d).cpu().double().numpy()
+        ref = O.decode_batched(np64(q), np64(kc), np64(vc), np64(bias), G, oracle_scale(p))
+        for (b, h) in chains:
+            assert_close_rows(out[b, h * G:(h + 1) * G], ref[b, h * G:(h + 1) * G], tol, f"decode step {step}")
+
+
+# ------------------------------------------------------------------ workloads at full size
+def test_tiny_workload_stagewise_and_decode(S):
+    w = synth.WORKLOADS["tiny"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    _, chains = run_stagewise(S, p, t["K"], t["V"], t["Qwin"])
+    run_decode_check(S, p, chains, t["K"], steps=w.decode_steps)
+
+
+def test_llama_layer_stagewise_and_decode(S):
+    w = synth.WORKLOADS["llama_layer"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    _, chains = run_stagewise(S, p, t["K"], t["V"], t["Qwin"])
+    run_decode_check(S, p, chains, t["K"], steps=4)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama_layer"])
+def test_end_to_end_with_near_tie_accounting(S, name):
+    """The full GPU pipeline on raw inputs.  Selection may differ from the
+    oracle only by swaps between candidates within eps of the threshold;
+    for every head whose kept set matches, all outputs are checked."""
+    w = synth.WORKLOADS[name]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
+    tol = TOL[w.dtype]
+    counts = []
+    for b in range(w.batch):
+        for h in range(w.n_heads_kv):
+            ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * w.group:(h + 1) * w.group],
+                                 window=w.window, budget_ratio=p.budget_ratio)
+            assert_close_elem(np64(comp.attn[b, h]), ch["attn"], SCORE_RTOL, "attn")
+            assert_close_elem(np64(comp.score[b, h]), ch["score"], SCORE_RTOL, "score")
+            counts.append(compare_end_to_end(gpu_head(comp, b, h), ch, K64[b, h], w.seq_len, p.bucket, tol,
+                                             float(np.float32(p.alpha))))
+    print(f"{name}: near-tie counts per head: {counts}")
+
+
+# ------------------------------------------------------------------ edge cases, ragged shapes, modes
+EDGE = [
+    dict(batch=1, H=2, G=2, d=64, n=1000, W=32, dtype="fp32"),                 # ragged n
+    dict(batch=2, H=1, G=3, d=128, n=77, W=20, dtype="bf16"),                  # odd G, tiny n
+    dict(batch=1, H=2, G=1, d=128, n=17, W=17, dtype="fp32"),                  # W = n
+    dict(batch=1, H=1, G=4, d=64, n=300, W=32, dtype="bf16", budget_ratio=1.0),   # identity
+    dict(batch=1, H=2, G=2, d=128, n=200, W=8, dtype="fp32", budget_ratio=0.05),  # m < m_r
+    dict(batch=1, H=1, G=2, d=64, n=513, W=32, dtype="bf16", gate_mode=1),     # drop
+    dict(batch=1, H=1, G=2, d=64, n=513, W=32, dtype="bf16", gate_mode=2),     # merge all
+    dict(batch=1, H=2, G=2, d=128, n=400, W=16, dtype="fp32", bucket=4, budget_ratio=0.1),  # empty buckets
+    dict(batch=1, H=1, G=2, d=64, n=333, W=32, dtype="fp32", pool_kernel=1, recent=0, bucket=64),
+    dict(batch=1, H=1, G=2, d=64, n=333, W=32, dtype="bf16", pool_kernel=7, bucket=1),
+    dict(batch=1, H=1, G=8, d=128, n=640, W=64, dtype="bf16"),                 # 512 window rows: row groups
+    dict(batch=1, H=1, G=5, d=128, n=256, W=40, dtype="fp32"),                 # fp32 row groups
+    dict(batch=1, H=2, G=2, d=64, n=400, W=32, dtype="bf16", gate_threshold=0.3, gate_temperature=0.25, alpha=1.0),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[f"edge{i}" for i in range(len(EDGE))])
+def test_edge_cases_stagewise(S, case):
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] + case["d"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"], device=DEV)
+    K, V = t["K"], t["V"]
+    if case["n"] > 50:   # a few zero value rows: norm 0 -> sim 0
+        V[:, :, 5].zero_()
+        V[:, :, 40].zero_()
+    p = make_params(S, case, **kw)
+    _, chains = run_stagewise(S, p, K, V, t["Qwin"])
+    run_decode_check(S, p, chains, K, steps=2)
+
+
+def test_mha_sweep_budgets_and_gates(S):
+    """Config-5 shape (MHA, W = 64) at reduced n: every budget, and the 9
+    gate settings on shared scores, stage-wise through merge and bias."""
+    w = synth.WORKLOADS["mha_sweep"].replace(seq_len=2048, batch=2, n_heads_kv=4)
+    t = synth.make_layer(w, 0, DEV)
+    for rho in w.budgets:
+        for (tau, T) in w.gate_sweep:
+            p = make_params(S, case_from_workload(w), budget_ratio=rho, gate_threshold=tau, gate_temperature=T)
+            run_stagewise(S, p, t["K"], t["V"], t["Qwin"], heads=[(0, 0), (1, 3)])
+
+
+# ------------------------------------------------------------------ determinism, bias semantics
+def test_bitwise_determinism_and_zero_bias(S):
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096)
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    c1 = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"]).outputs()
+    c2 = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"]).outputs()
+    torch.cuda.synchronize()
+    for k in c1:
+        assert torch.equal(c1[k], c2[k]), k
+    m = c1["K_out"].shape[2]
+    dec = S.Decoder(p, m, DEV)
+    q = synth.make_decode_queries(w, 0, 2, DEV)[0]
+    o_null = dec.run(q, c1["K_out"], c1["V_out"], None).clone()
+    o_zero = dec.run(q, c1["K_out"], c1["V_out"], torch.zeros_like(c1["bias"])).clone()
+    o_b1 = dec.run(q, c1["K_out"], c1["V_out"], c1["bias"]).clone()
+    o_b2 = dec.run(q, c1["K_out"], c1["V_out"], c1["bias"]).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(o_null, o_zero)
+    assert torch.equal(o_b1, o_b2)
+    assert not torch.equal(o_b1, o_null)
+
+
+def test_full_budget_identity_on_gpu(S):
+    """rho = 1: kept = all, K~ = K and V~ = V bitwise, bias = 0, and decode
+    equals full-cache decode bitwise (same kernel, same cache)."""
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=1024)
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w), budget_ratio=1.0)
+    c = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    assert torch.equal(c.kept.cpu(), torch.arange(1024, dtype=torch.int32).expand(1, 8, 1024))
+    assert torch.equal(c.K_out, t["K"]) and torch.equal(c.V_out, t["V"])
+    assert (c.bias == 0).all()
+    q = synth.make_decode_queries(w, 0, 1, DEV)[0]
+    dec = S.Decoder(p, 1024, DEV)
+    a = dec.run(q, c.K_out, c.V_out, c.bias).clone()
+    b = dec.run(q, t["K"], t["V"], None).clone()
+    assert torch.equal(a, b)
+    ref = O.decode_batched(np64(q), np64(t["K"]), np64(t["V"]), None, 4, 1 / math.sqrt(128))
+    assert_close_rows(a.cpu().double().numpy(), ref, TOL["bf16"], "decode")
+
+
+# ------------------------------------------------------------------ full sizes, bench launch configuration
+def _layers(w, n_layers, device):
+    """All layers' caches back to back as one batch [L*B, H, n, d]."""
+    L = n_layers
+    t0 = synth.make_layer(w, 0, device)
+    K = torch.empty((L,) + tuple(t0["K"].shape), dtype=t0["K"].dtype, device=device)
+    V = torch.empty_like(K)
+    Q = torch.empty((L,) + tuple(t0["Qwin"].shape), dtype=t0["Qwin"].dtype, device=device)
+    for layer in range(L):
+        t = t0 if layer == 0 else synth.make_layer(w, layer, device)
+        K[layer], V[layer], Q[layer] = t["K"], t["V"], t["Qwin"]
+    return K.flatten(0, 1), V.flatten(0, 1), Q.flatten(0, 1)
+
+
+@pytest.mark.parametrize("name,samples", [("ctx32k", [(0, 0), (31, 7)]), ("ctx100k", [(0, 3), (31, 6)])])
+def test_full_size_all_layers_sampled(S, name, samples):
+    """The bench's launch: every layer of the cache compressed by one call
+    per step (batch = layers).  Sampled (layer, head) slices are checked
+    end-to-end against the oracle run on that slice alone."""
+    w = synth.WORKLOADS[name]
+    K, V, Q = _layers(w, w.layers, DEV)
+    p = make_params(S, case_from_workload(w), batch=w.layers * w.batch)
+    comp = S.Compressor(p, DEV).run(K, V, Q)
+    torch.cuda.synchronize()
+    tol = TOL[w.dtype]
+    for (layer, h) in samples:
+        K64, V64 = np64(K[layer, h]), np64(V[layer, h])
+        Q64 = np64(Q[layer, h * w.group:(h + 1) * w.group])
+        ch = O.compress_head(K64, V64, Q64, window=w.window, budget_ratio=p.budget_ratio)
+        assert_close_elem(np64(comp.attn[layer, h]), ch["attn"], SCORE_RTOL, "attn")
+        assert_close_elem(np64(comp.vnorm[layer, h]), ch["vnorm"], SCORE_RTOL, "vnorm")
+        s_gpu = np64(comp.score[layer, h])
+        assert_close_elem(s_gpu, ch["score"], SCORE_RTOL, "score")
+        counts = compare_end_to_end(gpu_head(comp, layer, h), ch, K64, w.seq_len, p.bucket, tol,
+                                    float(np.float32(p.alpha)))
+        print(f"{name} layer {layer} head {h}: {counts}")
+        # biased decode on this layer's compressed cache vs the oracle (2 steps)
+        qd = synth.make_decode_queries(w, layer, 2, DEV)
+        dec = S.Decoder(S.params(batch=1, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim,
+                                 kv_dtype=w.dtype), ch["m"], DEV)
+        for st in range(2):
+            out = dec.run(qd[st], comp.K_out[layer:layer + 1], comp.V_out[layer:layer + 1],
+                          comp.bias[layer:layer + 1]).cpu().double().numpy()[0, h * w.group:(h + 1) * w.group]
+            ref = O.decode(np64(qd[st][0, h * w.group:(h + 1) * w.group]), np64(comp.K_out[layer, h])[None],
+                           np64(comp.V_out[layer, h])[None], np64(comp.bias[layer, h])[None], w.group,
+                           1 / math.sqrt(w.head_dim))
+            assert_close_rows(out, ref, tol, "decode")
+
+
+def test_full_cache_decode_100k(S):
+    """The comparison decode of the long-context point: the whole 102400-entry
+    cache, no bias, sampled heads against the oracle."""
+    w = synth.WORKLOADS["ctx100k"]
+    t = synth.make_layer(w, 5, DEV)
+    p = S.params(batch=1, n_heads_kv=8, group=4, head_dim=128, kv_dtype="bf16")
+    dec = S.Decoder(p, w.seq_len, DEV)
+    q = synth.make_decode_queries(w, 5, 2, DEV)
+    for st in range(2):
+        out = dec.run(q[st], t["K"], t["V"], None).cpu().double().numpy()[0]
+        for h in (0, 7):
+            ref = O.decode(np64(q[st][0, 4 * h:4 * h + 4]), np64(t["K"][0, h])[None], np64(t["V"][0, h])[None],
+                           None, 4, 1 / math.sqrt(128))
+            assert_close_rows(out[4 * h:4 * h + 4], ref, TOL["bf16"], "full decode")
+
+
+def test_abi_errors_with_device_memory(S):
+    w = synth.WORKLOADS["tiny"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    c = S.Compressor(p, DEV)
+    small = torch.empty(16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(S.SelkvError) as e:
+        S.score(p, t["K"], t["V"], t["Qwin"], c.score, c.attn, c.vnorm, small)
+    assert e.value.status == 5
+    raw = torch.empty(t["K"].numel() * 4 + 16, dtype=torch.uint8, device=DEV)
+    import ctypes
+    st = S.lib.selkv_score(ctypes.byref(p), ctypes.c_void_p(raw.data_ptr() + 4), ctypes.c_void_p(t["V"].data_ptr()),
+                           ctypes.c_void_p(t["Qwin"].data_ptr()), ctypes.c_void_p(c.score.data_ptr()),
+                           ctypes.c_void_p(c.attn.data_ptr()), ctypes.c_void_p(c.vnorm.data_ptr()),
+                           ctypes.c_void_p(c.ws_score.data_ptr()), c.ws_score.numel(), None)
+    assert st == 4
+    torch.cuda.synchronize()
