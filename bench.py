@@ -1,0 +1,340 @@
+#!/usr/bin/env python3
+"""SelKV hot path on one MI355X: one-shot compression of a whole model's KV
+cache plus biased decode over the compressed caches.
+
+One step = compress every layer of the synthetic cache (score -> select ->
+merge -> bias, one call each with the layers as the batch) and then run the
+workload's decode steps, each of which calls the biased decode once per
+layer with fresh queries (captured once into a HIP graph and replayed).
+Inputs are resident in HBM before the timed region starts.
+
+Prints one JSON line: compress tokens/s at the long-context point (value),
+the 32k point, decode microseconds per layer and per token, the full-cache
+decode comparison, per-stage achieved bandwidth, the roofline of the
+dominant kernel (decode) and the float64 CPU oracle timed on a sample.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+METRIC = "SelKV compress tokens/s @32k,100k; biased-decode step µs; % HBM/MFMA peak"
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_ctx100k_pmc.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="ctx100k")
+    ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload's)")
+    ap.add_argument("--no-32k", action="store_true", help="skip the 32k-context secondary point")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=6, help="(layer, head) slices the oracle compresses")
+    ap.add_argument("--no-graph", action="store_true", help="launch decode eagerly instead of from a HIP graph")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (counter calibration for profiling passes)")
+    return ap.parse_args()
+
+
+def source_hash(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def read_traffic(decode_src):
+    """HBM traffic per decode launch from the committed counter summary, or
+    None when it is missing or was taken on a different kernel source."""
+    try:
+        kv = {}
+        for line in open(PMC_SUMMARY):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("decode_source_sha256") != source_hash(decode_src):
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+class Job:
+    """Resident inputs, outputs and decode graph of one workload."""
+
+    def __init__(self, w, dev, decode_steps, use_graph, full_cache_decode):
+        import torch
+        from paper_2607_16213_amd import selkv, synth
+        self.torch, self.selkv = torch, selkv
+        self.w = w
+        L, B, H, G, d, n = w.layers, w.batch, w.n_heads_kv, w.group, w.head_dim, w.seq_len
+        self.LB = L * B
+        t0 = synth.make_layer(w, 0, dev)
+        self.K = torch.empty((L,) + tuple(t0["K"].shape), dtype=t0["K"].dtype, device=dev)
+        self.V = torch.empty_like(self.K)
+        self.Q = torch.empty((L,) + tuple(t0["Qwin"].shape), dtype=t0["Qwin"].dtype, device=dev)
+        self.T = decode_steps
+        self.Qd = torch.empty((decode_steps, L, B, H * G, d), dtype=t0["K"].dtype, device=dev)
+        for layer in range(L):
+            t = t0 if layer == 0 else synth.make_layer(w, layer, dev)
+            self.K[layer], self.V[layer], self.Q[layer] = t["K"], t["V"], t["Qwin"]
+            self.Qd[:, layer] = synth.make_decode_queries(w, layer, decode_steps, dev)
+        del t0
+        self.Kf, self.Vf, self.Qf = self.K.flatten(0, 1), self.V.flatten(0, 1), self.Q.flatten(0, 1)
+        self.p = selkv.params(batch=self.LB, n_heads_kv=H, group=G, head_dim=d, seq_len=n, window=w.window,
+                              kv_dtype=w.dtype, budget_ratio=w.budgets[0])
+        self.comp = selkv.Compressor(self.p, dev)
+        self.m = self.comp.m
+        self.pd = selkv.params(batch=B, n_heads_kv=H, group=G, head_dim=d, kv_dtype=w.dtype)
+        self.dec = selkv.Decoder(self.pd, self.m, dev)
+        self.outs = torch.empty((L, B, H * G, d), dtype=torch.float32, device=dev)
+        self.graph = None
+        self.full_dec = selkv.Decoder(self.pd, n, dev) if full_cache_decode else None
+        self.use_graph = use_graph
+
+    # -- one call per stage, whole model as the batch
+    def compress(self, ev=None):
+        s, c, p = self.selkv, self.comp, self.p
+        if ev: ev[0].record()
+        s.score(p, self.Kf, self.Vf, self.Qf, c.score, c.attn, c.vnorm, c.ws_score)
+        if ev: ev[1].record()
+        s.select(p, c.score, c.kept, c.evicted)
+        if ev: ev[2].record()
+        s.merge(p, self.Kf, self.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
+                c.ws_merge)
+        if ev: ev[3].record()
+        s.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, c.ws_bias)
+        if ev: ev[4].record()
+
+    def _decode_eager(self, steps):
+        c, B = self.comp, self.w.batch
+        for t in range(steps):
+            for layer in range(self.w.layers):
+                sl = slice(layer * B, (layer + 1) * B)
+                self.dec.run(self.Qd[t, layer], c.K_out[sl], c.V_out[sl], c.bias[sl], out=self.outs[layer])
+
+    def build_graph(self):
+        """Capture the whole decode loop once; replays are checked bitwise
+        against the eager loop, with eager work between replays."""
+        torch = self.torch
+        self._decode_eager(self.T)
+        torch.cuda.synchronize()
+        ref = self.outs.clone()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self._decode_eager(1)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            self._decode_eager(self.T)
+        for _ in range(2):
+            self.outs.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            if not torch.equal(self.outs, ref):
+                raise RuntimeError("decode graph replay differs from the eager decode")
+            self._decode_eager(1)              # eager work between replays
+            torch.cuda.synchronize()
+        self.graph = g
+
+    def decode(self):
+        if self.graph is not None:
+            self.graph.replay()
+        else:
+            self._decode_eager(self.T)
+
+    def full_decode(self, reps):
+        """Decode over the uncompressed n-entry cache (no bias), cycling layers."""
+        B = self.w.batch
+        for r in range(reps):
+            layer = r % self.w.layers
+            sl = slice(layer * B, (layer + 1) * B)
+            self.full_dec.run(self.Qd[r % self.T, layer], self.Kf[sl], self.Vf[sl], None, out=self.outs[layer])
+
+
+def stage_bytes(w, m):
+    """Algorithmic bytes of each call over the whole-model batch (each input
+    read once, each output written once; workspace excluded)."""
+    L, B, H, G, d, n, W = w.layers, w.batch, w.n_heads_kv, w.group, w.head_dim, w.seq_len, w.window
+    e = 2 if w.dtype == "bf16" else 4
+    heads = L * B * H
+    mr = min(16, m)
+    ev = n - m
+    score = heads * (2 * n * d * e + G * W * d * e + 4 * (n - mr) + 8 * n)
+    select = heads * (4 * (n - mr) + 4 * n)
+    merge = heads * (n * d * e + m * d * e + 8 * n + 4 * n + 2 * m * d * e + 8 * ev)
+    bias = heads * (4 * m + 4 * ev + 4 * ev + 8 * ev + 4 * m)
+    per_decode = B * H * (2 * m * d * e + 4 * m) + B * H * G * d * (e + 4)
+    full_decode = B * H * (2 * n * d * e) + B * H * G * d * (e + 4)
+    return dict(score=score, select=select, merge=merge, bias=bias), per_decode, full_decode
+
+
+def cpu_baseline(job, n_heads, dev):
+    """The float64 oracle, as it stands, on sampled (layer, head) slices of
+    the same workload, single-threaded; scaled to the whole job."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import selkv_oracle as O
+    w, torch = job.w, job.torch
+    rng = np.random.default_rng(2607)
+    picks = [(int(rng.integers(w.layers)), int(rng.integers(w.n_heads_kv))) for _ in range(n_heads)]
+    f64 = lambda x: x.detach().double().cpu().numpy()
+    t_comp, outs = 0.0, []
+    with threadpool_limits(1):
+        for (layer, h) in picks:
+            K, V = f64(job.K[layer, 0, h]), f64(job.V[layer, 0, h])
+            Q = f64(job.Q[layer, 0, h * w.group:(h + 1) * w.group])
+            t0 = time.perf_counter()
+            r = O.compress_head(K, V, Q, window=w.window, budget_ratio=w.budgets[0])
+            t_comp += time.perf_counter() - t0
+            outs.append((layer, h, r))
+        t_dec, nd = 0.0, 0
+        for (layer, h, r) in outs:
+            for st in range(4):
+                q = f64(job.Qd[st, layer, 0, h * w.group:(h + 1) * w.group])
+                t0 = time.perf_counter()
+                O.decode(q, r["k_out"][None], r["v_out"][None], r["bias"][None], w.group, 1 / math.sqrt(w.head_dim))
+                t_dec += time.perf_counter() - t0
+                nd += 1
+    per_head = t_comp / len(picks)
+    heads_total = w.layers * w.batch * w.n_heads_kv
+    return {
+        "value": w.seq_len * w.batch / (per_head * heads_total),
+        "unit": "tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"float64 oracle compress_head on {len(picks)} (layer, KV head) slices of {w.name} "
+                  f"(n={w.seq_len}), scaled to {heads_total} slices; decode on {nd} (slice, step) samples",
+        "seconds": round(t_comp + t_dec, 2),
+        "decode_us_per_layer_step": 1e6 * (t_dec / nd) * w.n_heads_kv,
+    }
+
+
+def measure(job, steps, warmup):
+    torch = job.torch
+    for _ in range(warmup):
+        job.compress()
+        job.decode()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        ev = evs[s]
+        job.compress(ev)
+        job.decode()
+        ev[5].record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    st = {k: 0.0 for k in ("score", "select", "merge", "bias", "decode")}
+    for ev in evs:
+        for i, k in enumerate(("score", "select", "merge", "bias", "decode")):
+            st[k] += ev[i].elapsed_time(ev[i + 1]) / steps      # ms
+    return wall, st
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one MI355X only (every SelKV step is independent per layer and "
+              "KV head, and no multi-GPU path is built); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_16213_amd import synth
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+
+    w = synth.WORKLOADS[args.workload]
+    T = w.decode_steps if args.decode_steps is None else args.decode_steps
+    job = Job(w, dev, T, not args.no_graph, w.decode_cache_full)
+    if job.use_graph:
+        job.compress()
+        job.build_graph()
+    wall, st = measure(job, args.steps, args.warmup)
+    sb, per_decode, full_decode_bytes = stage_bytes(w, job.m)
+    comp_ms = st["score"] + st["select"] + st["merge"] + st["bias"]
+    value = w.seq_len * w.batch / (comp_ms / 1e3)
+    n_dec = T * w.layers
+    dec_us = st["decode"] * 1e3 / n_dec
+    decode_gbs = per_decode / (dec_us * 1e-6) / 1e9
+
+    stages = {}
+    for k in ("score", "select", "merge", "bias"):
+        gbs = sb[k] / (st[k] * 1e-3) / 1e9
+        stages[k] = {"ms": round(st[k], 4), "alg_bytes": sb[k], "achieved_GBs": round(gbs, 1),
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    stages["decode"] = {"us_per_launch": round(dec_us, 3), "alg_bytes_per_launch": per_decode,
+                        "achieved_GBs": round(decode_gbs, 1), "frac_hbm": round(decode_gbs / HBM_PEAK_GBS, 4)}
+
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(wall * 1e3, 3), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+           "config": {"workload": w.name, "layers": w.layers, "batch": w.batch, "heads_q": w.n_heads_q,
+                      "heads_kv": w.n_heads_kv, "head_dim": w.head_dim, "seq_len": w.seq_len, "window": w.window,
+                      "budget_ratio": w.budgets[0], "decode_steps": T, "retained_per_kv_head": job.m,
+                      "decode_launch": "hip_graph" if job.graph is not None else "eager"},
+           "compress_ms": round(comp_ms, 4),
+           "decode_us_per_layer_step": round(dec_us, 3),
+           "decode_us_per_token": round(dec_us * w.layers, 2),
+           "stages": stages}
+
+    if job.full_dec is not None:
+        reps = 4 * w.layers
+        job.full_decode(w.layers)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        job.full_decode(reps)
+        e1.record()
+        torch.cuda.synchronize()
+        full_us = e0.elapsed_time(e1) * 1e3 / reps
+        out["full_cache_decode_us_per_layer_step"] = round(full_us, 3)
+        out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
+        out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
+
+    decode_src = os.path.join(ROOT, "paper_2607_16213_amd", "csrc", "decode.hip")
+    traffic = read_traffic(decode_src)
+    out["roofline"] = {"kernel": "decode_split_kernel", "bound": "hbm", "achieved": round(decode_gbs, 1),
+                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_gbs / HBM_PEAK_GBS, 4),
+                       "traffic": traffic, "alg_bytes_per_launch": per_decode}
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    if not args.no_32k and w.name != "ctx32k":
+        w32 = synth.WORKLOADS["ctx32k"]
+        j32 = Job(w32, dev, w32.decode_steps if args.decode_steps is None else min(args.decode_steps, w32.decode_steps),
+                  not args.no_graph, False)
+        if j32.use_graph:
+            j32.compress()
+            j32.build_graph()
+        _, st32 = measure(j32, max(1, args.steps), 1)
+        c32 = st32["score"] + st32["select"] + st32["merge"] + st32["bias"]
+        sb32, pd32, _ = stage_bytes(w32, j32.m)
+        d32 = st32["decode"] * 1e3 / (j32.T * w32.layers)
+        out["ctx32k"] = {"compress_tokens_per_s": round(w32.seq_len / (c32 / 1e3), 1), "compress_ms": round(c32, 4),
+                         "decode_us_per_layer_step": round(d32, 3),
+                         "decode_GBs": round(pd32 / (d32 * 1e-6) / 1e9, 1),
+                         "score_GBs": round(sb32["score"] / (st32["score"] * 1e-3) / 1e9, 1),
+                         "merge_GBs": round(sb32["merge"] / (st32["merge"] * 1e-3) / 1e9, 1)}
+        del j32
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(job, args.cpu_heads, dev)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

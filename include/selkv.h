@@ -19,8 +19,8 @@
  *  - Storage dtype of K, V and queries is params.kv_dtype (fp32 or bf16);
  *    all arithmetic accumulates in fp32.  Scores, attention masses, norms,
  *    gates and biases are fp32; indices are int32.
- *  - K, V and query pointers must be 16-byte aligned; fp32 / int32 arrays
- *    4-byte aligned.
+ *  - K, V, query and decode-output pointers must be 16-byte aligned; other
+ *    fp32 / int32 arrays 4-byte aligned.
  *  - Calls are asynchronous on `stream` (0 = the null stream) and never
  *    synchronise the host.  Arguments are validated on the host before
  *    anything is launched; an invalid call returns an error status and
@@ -205,12 +205,16 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
  * out[b, h] = sum_s softmax_s(scale * q[b, h] . K[b, h/G, s] + bias[b, h/G, s]) V[b, h/G, s]
  * over the cache_len entries of KV head h/G.  bias may be NULL (plain
  * attention, e.g. the uncompressed cache); a zero bias gives bitwise the
- * same result as NULL.  Split-K over the cache with an in-order combine.
+ * same result as NULL.  Split-K over the cache with an in-order combine in
+ * the same launch.
  * In:  q [B, H_kv*G, d] (kv_dtype); K, V [B, H_kv, cache_len, d] (kv_dtype);
  *      bias [B, H_kv, cache_len] fp32 or NULL.  Uses params batch,
- *      n_heads_kv, group, head_dim, kv_dtype and scale only.
+ *      n_heads_kv, group (1..8), head_dim, kv_dtype and scale only.
  * Out: out [B, H_kv*G, d] fp32.
- * Workspace: selkv_workspace_size(p, SELKV_CALL_DECODE, cache_len). */
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_DECODE, cache_len) bytes.
+ *      It holds per-head completion counters and MUST be zero-filled before
+ *      its first use; every call leaves the counters at zero again.  Calls
+ *      that may overlap in time need separate workspaces. */
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream);

@@ -91,12 +91,19 @@ template <> struct Mma<float> {
 __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, 64); }
 __device__ __forceinline__ int xor_shfl(int v, int mask) { return __shfl_xor(v, mask, 64); }
 
-// Sum over the 16 lanes of a lane group (lanes 16q .. 16q+15), same result on all of them.
+// Lane i of a 16-lane row reads lane (i + n) mod 16 of the same row (DPP row_ror).
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
+}
+
+// Sum over the 16 lanes of a lane group (lanes 16q .. 16q+15) with DPP row
+// rotations; every lane of the group ends with the bitwise-same total.
 __device__ __forceinline__ float sum16(float v) {
-  v += xor_shfl(v, 1);
-  v += xor_shfl(v, 2);
-  v += xor_shfl(v, 4);
-  v += xor_shfl(v, 8);
+  v += row_ror<8>(v);
+  v += row_ror<4>(v);
+  v += row_ror<2>(v);
+  v += row_ror<1>(v);
   return v;
 }
 

@@ -142,14 +142,24 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   const int k0 = oh[bucket], k1 = oh[bucket + 1];
   const int e0 = start - k0, e1 = end - k1;
   if (k0 > k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // inconsistent kept list
+  const int nk = k1 - k0, ne = e1 - e0;   // both <= B <= 64
+
+  // lane-parallel metadata of the bucket: lane i holds kept entry i and evicted entry i
+  int pos_k = 0, pos_e = 0;
+  float a_k = kNegInf, a_e = 0.f, vn_e = 0.f;
+  if (lane < nk) {
+    pos_k = kh[k0 + lane];
+    a_k = ah[pos_k];
+  }
+  if (lane < ne) {
+    pos_e = eh[e0 + lane];
+    a_e = ah[pos_e];
+    vn_e = vnh[pos_e];
+  }
 
   // route: kept token of the bucket with the largest attention, lowest slot on ties
-  float best_a = kNegInf;
-  int best = 0x7fffffff;
-  if (lane < k1 - k0) {
-    best_a = ah[kh[k0 + lane]];
-    best = lane;
-  }
+  float best_a = a_k;
+  int best = lane < nk ? lane : 0x7fffffff;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const float oa = xor_shfl(best_a, off);
@@ -159,14 +169,14 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
       best = ob;
     }
   }
-  const int tslot = (k1 > k0) ? k0 + best : -1;
+  const int tslot = nk > 0 ? k0 + best : -1;
+  const int tpos = __shfl(pos_k, nk > 0 ? best : 0, 64);
+  const float a_t = nk > 0 ? best_a : 0.f;
 
   float vt[E];
-  float a_t = 0.f, vn_t = 0.f;
+  float vn_t = 0.f;
   if (tslot >= 0) {
-    const int tpos = kh[tslot];
     load_slice<T, D>(Vh + (size_t)tpos * RB, col, vt);
-    a_t = ah[tpos];
     vn_t = vnh[tpos];
   } else {
 #pragma unroll
@@ -177,13 +187,16 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   float wsum = 0.f;
-  for (int eb = e0; eb < e1; eb += 4) {
-    const int ei = eb + grp;
-    const bool valid = ei < e1;
+#pragma unroll 2
+  for (int ib = 0; ib < ne; ib += 4) {     // uniform trip count; lane group q takes entry ib + q
+    const int i = ib + grp;
+    const bool valid = i < ne;
+    const int src = valid ? i : 0;
+    const int j = __shfl(pos_e, src, 64);
+    const float aj = __shfl(a_e, src, 64);
+    const float vnj = __shfl(vn_e, src, 64);
     float vj[E];
-    int j = 0;
     if (valid) {
-      j = eh[ei];
       load_slice<T, D>(Vh + (size_t)j * RB, col, vj);
     } else {
 #pragma unroll
@@ -193,26 +206,23 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
 #pragma unroll
     for (int e = 0; e < E; ++e) dot = fmaf(vj[e], vt[e], dot);
     dot = sum16(dot);
-    if (valid) {
-      float g = 0.f;
-      if (tslot >= 0) {
-        if (a.gate_mode == SELKV_GATE_DROP) {
-          g = 0.f;
-        } else if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
-          g = 1.f;
-        } else {
-          const float vn_j = vnh[j];
-          const float sim = (vn_j > 0.f && vn_t > 0.f) ? dot / (vn_j * vn_t) : 0.f;
-          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
-        }
-        const float w = g * ah[j];
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vj[e], acc[e]);
-        wsum += w;
+    float g = 0.f;
+    if (tslot >= 0) {
+      if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
+        g = 1.f;
+      } else if (a.gate_mode == SELKV_GATE_COSINE) {
+        const float sim = (vnj > 0.f && vn_t > 0.f) ? dot / (vnj * vn_t) : 0.f;
+        g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
       }
+    }
+    if (valid) {
+      const float w = g * aj;
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vj[e], acc[e]);
+      wsum += w;
       if (col == 0) {
-        th[ei] = tslot;
-        gh[ei] = g;
+        th[e0 + i] = tslot;
+        gh[e0 + i] = g;
       }
     }
   }
@@ -226,10 +236,11 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   wsum += xor_shfl(wsum, 32);
 
   // write the bucket's kept rows: keys gathered, values copied or merged
-  for (int kb = k0; kb < k1; kb += 4) {
-    const int k = kb + grp;
-    if (k < k1) {
-      const int pos = kh[k];
+  for (int kb = 0; kb < nk; kb += 4) {
+    const int i = kb + grp;
+    const int pos = __shfl(pos_k, i < nk ? i : 0, 64);
+    if (i < nk) {
+      const int k = k0 + i;
       copy_slice<T, D>(Ko + (size_t)k * RB, Kh + (size_t)pos * RB, col);
       if (k == tslot && wsum > 0.f) {
         const float den = a_t + wsum;
@@ -256,8 +267,9 @@ struct BiasArgs {
   float alpha;
 };
 
-// One wave per bucket; lane i owns kept slot k0 + i of the bucket and sums
-// what was routed to it in ascending evicted order.
+// One wave per bucket.  Lane e loads the bucket's e-th evicted entry and its
+// contribution g * a (all loads in parallel); lane i then owns kept slot
+// k0 + i and adds, in ascending evicted order, the contributions routed to it.
 __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   const int64_t head = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -275,13 +287,22 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   const int k0 = oh[bucket], k1 = oh[bucket + 1];
   const int e0 = start - k0, e1 = end - k1;
   if (k0 > k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // inconsistent kept list
+  const int ne = e1 - e0;
+  int t_e = -1;
+  float c_e = 0.f;
+  if (lane < ne) {
+    t_e = th[e0 + lane];
+    c_e = gh[e0 + lane] * ah[eh[e0 + lane]];
+  }
   const int k = k0 + lane;
-  if (k >= k1) return;
+  const float ai = lane < k1 - k0 ? ah[kh[k]] : 1.f;
   float absorbed = 0.f;
-  for (int e = e0; e < e1; ++e)
-    if (th[e] == k) absorbed += gh[e] * ah[eh[e]];
-  const float ai = ah[kh[k]];
-  a.bias[(size_t)head * m + k] = absorbed > 0.f ? a.alpha * log1pf(absorbed / ai) : 0.f;
+  for (int i = 0; i < ne; ++i) {
+    const int t = __shfl(t_e, i, 64);
+    const float c = __shfl(c_e, i, 64);
+    if (t == k) absorbed += c;
+  }
+  if (k < k1) a.bias[(size_t)head * m + k] = absorbed > 0.f ? a.alpha * log1pf(absorbed / ai) : 0.f;
 }
 
 }  // namespace

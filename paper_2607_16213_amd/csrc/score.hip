@@ -3,15 +3,22 @@
 //
 // For one KV head the window rows are the G*W query rows of its G query
 // heads (row r = h*W + i is position n-W+i, causal).  The logits
-// scale * Q K^T are produced on MFMA (16x16x32 bf16, or 16x16x4 fp32) from
-// Q fragments held in registers and K streamed once per pass:
-//   pass 1  per (chunk of keys, row group): online row max / sum-exp  -> ws
+// scale * Q K^T are produced on MFMA (16x16x32 bf16, or 16x16x4 fp32) with
+// Q fragments in registers and K streamed from HBM:
+//   pass 1  per (key chunk, row group): online row max / sum of exp  -> ws
 //   combine per KV head: merge the chunk partials in chunk order     -> ws
-//   pass 2  per chunk: recompute the logits, normalise, sum the G*W rows
-//           of every key column (a_j, divided by G), read V for ||v_j||,
-//           write attn, vnorm and c = a * ||v||
+//   pass 2  per key chunk: recompute the logits, normalise, sum the G*W
+//           rows of every key column (a_j, divided by G), value norms from
+//           V, write attn, vnorm and c = a * ||v||
 //   pool    centred K-wide moving average of c over [0, n - m_r')
 // The attention matrix itself is never stored.
+//
+// Work split inside a 4-wave workgroup: RW waves share each K tile, each
+// holding NRB 16-row blocks of Q (RW * NRB * 16 rows per row group); the
+// 4 / RW pairs walk interleaved 16-key tiles of the chunk.  Every K load is
+// issued unconditionally (rows past the chunk end re-read its last row and
+// are masked) and the next tile is loaded before the current one is used.
+// Tiles that every row sees in full skip all masking.
 //
 // Fragment layout (both MFMA operands, all dtypes): lane l handles matrix
 // index l % 16 (a window row for Q, a key for K) and lane group g = l / 16
@@ -26,7 +33,8 @@ namespace {
 
 constexpr int kThreads = 256;          // 4 waves
 constexpr int kMaxChunkKeys = 4096;    // LDS column accumulator bound
-constexpr int kTargetBlocks = 4096;
+constexpr int kMinChunkKeys = 128;
+constexpr int kTargetBlocks = 2048;
 
 template <typename T, int D>
 struct Row {
@@ -59,7 +67,7 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
 }
 
 template <typename T, int D, int NRB>
-__device__ __forceinline__ void load_q(const ScoreArgs& a, const char* Qh, int row0, int col, int grp,
+__device__ __forceinline__ void load_q(const char* Qh, int R, int row0, int col, int grp,
                                        Chunk16 (&q)[NRB][Row<T, D>::kNch]) {
   constexpr int NCH = Row<T, D>::kNch;
 #pragma unroll
@@ -67,61 +75,76 @@ __device__ __forceinline__ void load_q(const ScoreArgs& a, const char* Qh, int r
     const int row = row0 + rb * 16 + col;
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
-      q[rb][c] = row < a.R ? load16(Qh + (size_t)row * Row<T, D>::kBytes + (c * 4 + grp) * 16) : zero16();
+      q[rb][c] = row < R ? load16(Qh + (size_t)row * Row<T, D>::kBytes + (c * 4 + grp) * 16) : zero16();
   }
 }
 
+// K (or V) fragments of the 16-key tile starting at t; keys past `last` re-read row `last`.
+template <typename T, int D>
+__device__ __forceinline__ void load_tile(const char* Xh, int t, int last, int col, int grp,
+                                          Chunk16 (&f)[Row<T, D>::kNch]) {
+  constexpr int NCH = Row<T, D>::kNch;
+  const int key = min(t + col, last);
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) f[c] = load16(Xh + (size_t)key * Row<T, D>::kBytes + (c * 4 + grp) * 16);
+}
+
 // Pass 1: per-row (max, sum of exp2) over this block's key chunk.
-template <typename T, int D, int NRB>
+template <typename T, int D, int NRB, int RW>
 __global__ __launch_bounds__(kThreads) void score_rowstats_kernel(ScoreArgs a) {
   constexpr int NCH = Row<T, D>::kNch;
-  constexpr int RB = Row<T, D>::kBytes;
+  constexpr int TS = 4 / RW;
+  constexpr int ROWS = RW * NRB * 16;
   const int chunk = blockIdx.x;
   const int64_t head = blockIdx.y;
   const int rg = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int n = a.n;
-  const char* Kh = a.K + (size_t)head * n * RB;
-  const char* Qh = a.Q + (size_t)head * a.R * RB;
-  const int row0 = rg * NRB * 16;
+  const int half = wave % RW, stream = wave / RW;
+  const int n = a.n, W = a.W;
+  const char* Kh = a.K + (size_t)head * n * Row<T, D>::kBytes;
+  const char* Qh = a.Q + (size_t)head * a.R * Row<T, D>::kBytes;
+  const int row0 = rg * ROWS + half * NRB * 16;
 
   Chunk16 q[NRB][NCH];
-  load_q<T, D, NRB>(a, Qh, row0, col, grp, q);
+  load_q<T, D, NRB>(Qh, a.R, row0, col, grp, q);
 
   float m[NRB][4], s[NRB][4];
-  int lim[NRB][4];  // last visible key of the row, -1 for padding rows
+  int wi[NRB][4];  // window index of the row, -1 for padding rows
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = row0 + rb * 16 + grp * 4 + i;
-      lim[rb][i] = row < a.R ? n - a.W + row % a.W : -1;
+      wi[rb][i] = row < a.R ? row % W : -1;
       m[rb][i] = kNegInf;
       s[rb][i] = 0.f;
     }
 
   const int kb = chunk * a.chunk_keys;
   const int ke = min(n, kb + a.chunk_keys);
-  for (int t = kb + wave * 16; t < ke; t += 64) {
-    const int key = t + col;
-    Chunk16 kf[NCH];
-#pragma unroll
-    for (int c = 0; c < NCH; ++c)
-      kf[c] = key < ke ? load16(Kh + (size_t)key * RB + (c * 4 + grp) * 16) : zero16();
+  const int full_end = min(ke, n - W + 1);     // keys below this are seen by every row
+  int t = kb + stream * 16;
+  Chunk16 kcur[NCH], knxt[NCH];
+  if (t < ke) load_tile<T, D>(Kh, t, ke - 1, col, grp, kcur);
+  for (; t < ke; t += TS * 16) {
+    load_tile<T, D>(Kh, t + TS * 16, ke - 1, col, grp, knxt);
+    const bool fast = t + 16 <= full_end;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) acc = Mma<T>::step(q[rb][c], kf[c], acc);
+      for (int c = 0; c < NCH; ++c) acc = Mma<T>::step(q[rb][c], kcur[c], acc);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        if (key < ke && key <= lim[rb][i]) {
+        const int key = t + col;
+        const bool valid = fast || (key < ke && wi[rb][i] >= 0 && key <= n - W + wi[rb][i]);
+        if (valid) {
           const float x = acc[i] * a.c2;
           const float dlt = x - m[rb][i];
           const float e = fast_exp2(-fabsf(dlt));
           if (dlt > 0.f) {
-            s[rb][i] = s[rb][i] * e + 1.f;
+            s[rb][i] = fmaf(s[rb][i], e, 1.f);
             m[rb][i] = x;
           } else {
             s[rb][i] += e;
@@ -129,6 +152,8 @@ __global__ __launch_bounds__(kThreads) void score_rowstats_kernel(ScoreArgs a) {
         }
       }
     }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) kcur[c] = knxt[c];
   }
 
   // merge the 16 lanes (keys) that share each row
@@ -143,124 +168,139 @@ __global__ __launch_bounds__(kThreads) void score_rowstats_kernel(ScoreArgs a) {
         lse_merge(m[rb][i], s[rb][i], m2, s2);
       }
 
-  __shared__ float2 red[4][NRB * 16];
+  __shared__ float2 red[TS][ROWS];
   if (col == 0) {
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) red[wave][rb * 16 + grp * 4 + i] = make_float2(m[rb][i], s[rb][i]);
+      for (int i = 0; i < 4; ++i)
+        red[stream][half * NRB * 16 + rb * 16 + grp * 4 + i] = make_float2(m[rb][i], s[rb][i]);
   }
   __syncthreads();
-  if (threadIdx.x < NRB * 16) {
-    const int r = threadIdx.x;
+  for (int r = threadIdx.x; r < ROWS; r += kThreads) {
     float mm = red[0][r].x, ss = red[0][r].y;
-    for (int w = 1; w < 4; ++w) lse_merge(mm, ss, red[w][r].x, red[w][r].y);
-    a.part[((size_t)head * a.nchunks + chunk) * a.rpad + row0 + r] = make_float2(mm, ss);
+#pragma unroll
+    for (int w = 1; w < TS; ++w) lse_merge(mm, ss, red[w][r].x, red[w][r].y);
+    a.part[((size_t)head * a.nchunks + chunk) * a.rpad + rg * ROWS + r] = make_float2(mm, ss);
   }
 }
 
 // Combine the chunk partials of every row, in chunk order: (max, 1/sum).
 __global__ __launch_bounds__(kThreads) void score_combine_kernel(ScoreArgs a) {
+  constexpr int kBatch = 8;   // partial loads in flight per thread
   const int64_t head = blockIdx.x;
   for (int row = threadIdx.x; row < a.rpad; row += blockDim.x) {
     const float2* p = a.part + (size_t)head * a.nchunks * a.rpad + row;
-    float M = kNegInf;
-    for (int c = 0; c < a.nchunks; ++c) M = fmaxf(M, p[(size_t)c * a.rpad].x);
-    float L = 0.f;
-    if (M != kNegInf)
-      for (int c = 0; c < a.nchunks; ++c) {
-        const float2 v = p[(size_t)c * a.rpad];
-        L += v.y * fast_exp2(v.x - M);
-      }
+    float M = kNegInf, L = 0.f;
+    for (int c0 = 0; c0 < a.nchunks; c0 += kBatch) {
+      float2 v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) v[u] = p[(size_t)min(c0 + u, a.nchunks - 1) * a.rpad];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u)
+        if (c0 + u < a.nchunks) lse_merge(M, L, v[u].x, v[u].y);
+    }
     a.stats[(size_t)head * a.rpad + row] = (row < a.R && L > 0.f) ? make_float2(M, 1.f / L) : make_float2(0.f, 0.f);
   }
 }
 
 // Pass 2: column sums of the normalised window attention, value norms, c.
-template <typename T, int D, int NRB>
+template <typename T, int D, int NRB, int RW>
 __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   constexpr int NCH = Row<T, D>::kNch;
-  constexpr int RB = Row<T, D>::kBytes;
   constexpr int EPC = Elem<T>::kPerChunk;
+  constexpr int TS = 4 / RW;
+  constexpr int ROWS = RW * NRB * 16;
   const int chunk = blockIdx.x;
   const int64_t head = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int n = a.n;
-  const char* Kh = a.K + (size_t)head * n * RB;
-  const char* Vh = a.V + (size_t)head * n * RB;
-  const char* Qh = a.Q + (size_t)head * a.R * RB;
+  const int half = wave % RW, stream = wave / RW;
+  const int n = a.n, W = a.W;
+  const char* Kh = a.K + (size_t)head * n * Row<T, D>::kBytes;
+  const char* Vh = a.V + (size_t)head * n * Row<T, D>::kBytes;
+  const char* Qh = a.Q + (size_t)head * a.R * Row<T, D>::kBytes;
   const float2* st = a.stats + (size_t)head * a.rpad;
   const int kb = chunk * a.chunk_keys;
   const int ke = min(n, kb + a.chunk_keys);
+  const int full_end = min(ke, n - W + 1);
 
-  __shared__ float colacc[kMaxChunkKeys];
+  __shared__ float colacc[RW][kMaxChunkKeys];
+  __shared__ float vn_l[kMaxChunkKeys];
 
   for (int rg = 0; rg < a.nrg; ++rg) {
-    const int row0 = rg * NRB * 16;
-    const bool last = rg == a.nrg - 1;
+    const int row0 = rg * ROWS + half * NRB * 16;
     Chunk16 q[NRB][NCH];
-    load_q<T, D, NRB>(a, Qh, row0, col, grp, q);
+    load_q<T, D, NRB>(Qh, a.R, row0, col, grp, q);
     float Mr[NRB][4], iL[NRB][4];
-    int lim[NRB][4];
+    int wi[NRB][4];
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = row0 + rb * 16 + grp * 4 + i;
         const float2 v = st[row];
-        Mr[rb][i] = v.x;
-        iL[rb][i] = v.y;
-        lim[rb][i] = row < a.R ? n - a.W + row % a.W : -1;
+        Mr[rb][i] = -v.x;          // stored negated: exponent = fma(acc, c2, -M)
+        iL[rb][i] = v.y;           // 0 for padding rows
+        wi[rb][i] = row < a.R ? row % W : -1;
       }
+    const bool norms = rg == 0 && half == 0;   // one wave per tile reads V once
 
-    for (int t = kb + wave * 16; t < ke; t += 64) {
+    int t = kb + stream * 16;
+    Chunk16 kcur[NCH], knxt[NCH];
+    if (t < ke) load_tile<T, D>(Kh, t, ke - 1, col, grp, kcur);
+    for (; t < ke; t += TS * 16) {
+      load_tile<T, D>(Kh, t + TS * 16, ke - 1, col, grp, knxt);
+      Chunk16 vf[NCH];
+      if (norms) load_tile<T, D>(Vh, t, ke - 1, col, grp, vf);
+      const bool fast = t + 16 <= full_end;
       const int key = t + col;
-      const bool kin = key < ke;
-      Chunk16 kf[NCH];
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
-        kf[c] = kin ? load16(Kh + (size_t)key * RB + (c * 4 + grp) * 16) : zero16();
       float cs = 0.f;
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) acc = Mma<T>::step(q[rb][c], kf[c], acc);
+        for (int c = 0; c < NCH; ++c) acc = Mma<T>::step(q[rb][c], kcur[c], acc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (kin && key <= lim[rb][i]) cs += fast_exp2(acc[i] * a.c2 - Mr[rb][i]) * iL[rb][i];
+        for (int i = 0; i < 4; ++i) {
+          const float p = fast_exp2(fmaf(acc[i], a.c2, Mr[rb][i])) * iL[rb][i];
+          const bool valid = fast || (key < ke && wi[rb][i] >= 0 && key <= n - W + wi[rb][i]);
+          cs += valid ? p : 0.f;
+        }
       }
       cs += xor_shfl(cs, 16);
       cs += xor_shfl(cs, 32);
       const int local = key - kb;
-      if (!last) {
-        if (grp == 0 && kin) colacc[local] = (rg == 0 ? 0.f : colacc[local]) + cs;
-      } else {
-        float total = cs;
-        if (a.nrg > 1 && kin) total = colacc[local] + cs;
+      if (grp == 0 && key < ke) colacc[half][local] = (rg == 0 ? 0.f : colacc[half][local]) + cs;
+      if (norms) {
         float ss = 0.f;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const Chunk16 vf = kin ? load16(Vh + (size_t)key * RB + (c * 4 + grp) * 16) : zero16();
+        for (int c = 0; c < NCH; ++c)
 #pragma unroll
           for (int e = 0; e < EPC; ++e) {
-            const float x = Elem<T>::get(vf, e);
+            const float x = Elem<T>::get(vf[c], e);
             ss = fmaf(x, x, ss);
           }
-        }
         ss += xor_shfl(ss, 16);
         ss += xor_shfl(ss, 32);
-        if (grp == 0 && kin) {
-          const float av = total / (float)a.G;
-          const float vn = sqrtf(ss);
-          const size_t o = (size_t)head * n + key;
-          a.attn[o] = av;
-          a.vnorm[o] = vn;
-          a.cbuf[o] = av * vn;
-        }
+        if (grp == 0 && key < ke) vn_l[local] = sqrtf(ss);
       }
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) kcur[c] = knxt[c];
     }
+  }
+  __syncthreads();
+  for (int k = kb + (int)threadIdx.x; k < ke; k += kThreads) {
+    const int local = k - kb;
+    float total = colacc[0][local];
+#pragma unroll
+    for (int h = 1; h < RW; ++h) total += colacc[h][local];
+    const float av = total / (float)a.G;
+    const float vn = vn_l[local];
+    const size_t o = (size_t)head * n + k;
+    a.attn[o] = av;
+    a.vnorm[o] = vn;
+    a.cbuf[o] = av * vn;
   }
 }
 
@@ -280,30 +320,31 @@ __global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* cbuf,
   score[(size_t)head * n_cand + j] = s / (float)K;
 }
 
-template <typename T, int D, int NRB>
+template <typename T, int D, int NRB, int RW>
 hipError_t launch_t(const Shape& s, const ScorePlan& p, ScoreArgs& a, float* score, int pool_kernel,
                     hipStream_t st) {
   const dim3 blk(kThreads);
-  hipLaunchKernelGGL((score_rowstats_kernel<T, D, NRB>), dim3(p.nchunks, (unsigned)s.heads, p.nrg), blk, 0, st, a);
+  hipLaunchKernelGGL((score_rowstats_kernel<T, D, NRB, RW>), dim3(p.nchunks, (unsigned)s.heads, p.nrg), blk, 0, st,
+                     a);
   hipLaunchKernelGGL(score_combine_kernel, dim3((unsigned)s.heads), blk, 0, st, a);
-  hipLaunchKernelGGL((score_colsum_kernel<T, D, NRB>), dim3(p.nchunks, (unsigned)s.heads), blk, 0, st, a);
+  hipLaunchKernelGGL((score_colsum_kernel<T, D, NRB, RW>), dim3(p.nchunks, (unsigned)s.heads), blk, 0, st, a);
   if (s.n_cand > 0)
     hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kThreads - 1) / kThreads, (unsigned)s.heads), blk, 0,
                        st, a.cbuf, score, s.n, s.n_cand, pool_kernel);
   return hipGetLastError();
 }
 
+// Row blocks per wave (NRB) and waves sharing a tile (RW) for each dtype / head dim.
 template <typename T, int D>
 hipError_t launch_d(const Shape& s, const ScorePlan& p, ScoreArgs& a, float* score, int pool_kernel,
                     hipStream_t st) {
-  switch (p.rows_per_group / 16) {
-    case 1: return launch_t<T, D, 1>(s, p, a, score, pool_kernel, st);
-    case 2: return launch_t<T, D, 2>(s, p, a, score, pool_kernel, st);
-    case 4: return launch_t<T, D, 4>(s, p, a, score, pool_kernel, st);
-    default: break;
+  switch (p.rows_per_group) {
+    case 16: return launch_t<T, D, 1, 1>(s, p, a, score, pool_kernel, st);
+    case 32: return launch_t<T, D, 2, 1>(s, p, a, score, pool_kernel, st);
+    case 64: return launch_t<T, D, 4, 1>(s, p, a, score, pool_kernel, st);
+    case 128: return launch_t<T, D, 4, 2>(s, p, a, score, pool_kernel, st);
+    default: return hipErrorInvalidValue;
   }
-  if constexpr (Row<T, D>::kNch * 8 <= 32) return launch_t<T, D, 8>(s, p, a, score, pool_kernel, st);
-  return hipErrorInvalidValue;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -312,22 +353,22 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 ScorePlan plan_score(const Shape& s, int dtype) {
   ScorePlan p{};
-  const int nch = s.d * (dtype == SELKV_BF16 ? 2 : 4) / 64;
-  int max_nrb = 32 / nch;          // keep Q fragments within 128 VGPRs
-  if (max_nrb > 8) max_nrb = 8;
-  const int need = (s.R + 15) / 16;
-  int nrb = 1;
-  while (nrb < need && nrb < max_nrb) nrb <<= 1;
-  p.rows_per_group = nrb * 16;
-  p.nrg = (s.R + p.rows_per_group - 1) / p.rows_per_group;
-  p.rpad = p.nrg * p.rows_per_group;
+  // up to 128 rows per row group (4 row blocks per wave, two waves per tile);
+  // fp32 with d = 128 keeps 32 rows so Q stays within 64 VGPRs per wave
+  const int max_rows = (dtype == SELKV_F32 && s.d == 128) ? 32 : 128;
+  int rows = 16;
+  while (rows < s.R && rows < max_rows) rows <<= 1;
+  p.rows_per_group = rows;
+  p.nrg = (s.R + rows - 1) / rows;
+  p.rpad = p.nrg * rows;
 
   const int64_t tiles = (s.n + 63) / 64;
   int64_t nchunks = (kTargetBlocks + s.heads - 1) / s.heads;
   if (nchunks > tiles) nchunks = tiles;
   if (nchunks < 1) nchunks = 1;
   int64_t ck = ((s.n + nchunks - 1) / nchunks + 63) / 64 * 64;
-  const int64_t min_ck = ((int64_t)s.n + 63) / 64 * 64 < 256 ? ((int64_t)s.n + 63) / 64 * 64 : 256;
+  const int64_t n64 = ((int64_t)s.n + 63) / 64 * 64;
+  const int64_t min_ck = n64 < kMinChunkKeys ? n64 : kMinChunkKeys;
   if (ck < min_ck) ck = min_ck;
   if (ck > kMaxChunkKeys) ck = kMaxChunkKeys;
   p.chunk_keys = (int)ck;

@@ -18,6 +18,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kPerThread = 4;
 constexpr int kChunk = kThreads * kPerThread;
+constexpr int kHistBatch = 8;   // score loads in flight per thread
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -64,9 +65,15 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
     for (int shift = 24; shift >= 0; shift -= 8) {
       for (int b = tid; b < 256; b += kThreads) hist[b] = 0;
       __syncthreads();
-      for (int j = tid; j < n_cand; j += kThreads) {
-        const uint32_t u = order_key(s[j]);
-        if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1);
+      for (int j0 = tid; j0 < n_cand; j0 += kThreads * kHistBatch) {
+        float v[kHistBatch];
+#pragma unroll
+        for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, n_cand - 1)];
+#pragma unroll
+        for (int u = 0; u < kHistBatch; ++u) {
+          const uint32_t key = order_key(v[u]);
+          if (j0 + u * kThreads < n_cand && (key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+        }
       }
       __syncthreads();
       if (wave == 0) {
@@ -112,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
       const int j = base + tid * kPerThread + e;
-      u[e] = j < n_cand ? order_key(s[j]) : 0u;
+      u[e] = order_key(s[min(j, n_cand - 1)]);   // clamped: no load behind a branch
       neq += (j < n_cand && u[e] == T) ? 1 : 0;
     }
     int eq_total;

@@ -209,7 +209,7 @@ SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, c
   const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
   if (heads > 65535) return SELKV_EUNSUPPORTED;
   if (!q || !K || !V || !out) return SELKV_EINVAL;
-  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(bias, 4) || !aligned(out, 4))
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(bias, 4) || !aligned(out, 16))
     return SELKV_EALIGN;
   const DecodePlan plan = plan_decode(heads, cache_len, p->head_dim, p->group);
   selkv_status st = check_ws(ws, ws_bytes, plan.bytes);

@@ -118,8 +118,9 @@ def workspace_bytes(p: Params, call: int, cache_len: int = 0) -> int:
 
 
 def workspace(p: Params, call: int, device, cache_len: int = 0) -> torch.Tensor:
+    """Scratch for `call`, zero-filled (the decode workspace must start at zero)."""
     nbytes = workspace_bytes(p, call, cache_len)
-    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
 
 
 def _ptr(t):

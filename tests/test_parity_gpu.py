@@ -372,3 +372,37 @@ def test_abi_errors_with_device_memory(S):
                            ctypes.c_void_p(c.ws_score.data_ptr()), c.ws_score.numel(), None)
     assert st == 4
     torch.cuda.synchronize()
+
+
+def test_decode_hip_graph_replays_match_eager(S):
+    """Decode captured in a HIP graph: every replay (with eager work and
+    synchronisation in between) equals the eager result bitwise; the
+    workspace counters stay consistent across graph and eager launches."""
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096)
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    c = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    dec = S.Decoder(S.params(batch=1, n_heads_kv=8, group=4, head_dim=128, kv_dtype="bf16"), c.m, DEV)
+    qs = synth.make_decode_queries(w, 0, 4, DEV)
+    outs = torch.zeros((4,) + tuple(dec.out.shape), dtype=torch.float32, device=DEV)
+    for i in range(4):
+        dec.run(qs[i], c.K_out, c.V_out, c.bias, out=outs[i])
+    torch.cuda.synchronize()
+    ref = outs.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dec.run(qs[0], c.K_out, c.V_out, c.bias)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(4):
+            dec.run(qs[i], c.K_out, c.V_out, c.bias, out=outs[i])
+    for rep in range(3):
+        outs.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(outs, ref), f"replay {rep}"
+        dec.run(qs[1], c.K_out, c.V_out, None)       # eager work between replays
+        torch.cuda.synchronize()
