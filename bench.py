@@ -41,17 +41,26 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=6, help="(layer, head) slices the oracle compresses")
     ap.add_argument("--no-graph", action="store_true", help="launch decode eagerly instead of from a HIP graph")
+    ap.add_argument("--print-source-hash", action="store_true", help="print the decode source hash and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
     return ap.parse_args()
 
 
-def source_hash(path):
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2607_16213_amd", "csrc", f)
+                  for f in ("decode.hip", "common.hpp", "internal.hpp")]
 
 
-def read_traffic(decode_src):
-    """HBM traffic per decode launch from the committed counter summary, or
+def source_hash(paths=DECODE_SOURCES):
+    """Hash of the sources the decode kernels are built from."""
+    h = hashlib.sha256()
+    for p in paths:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM traffic per decode call from the committed counter summary, or
     None when it is missing or was taken on a different kernel source."""
     try:
         kv = {}
@@ -59,7 +68,7 @@ def read_traffic(decode_src):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
-        if kv.get("decode_source_sha256") != source_hash(decode_src):
+        if kv.get("decode_source_sha256") != source_hash():
             return None
         return float(kv["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
@@ -243,6 +252,9 @@ def measure(job, steps, warmup):
 
 def main():
     args = parse()
+    if args.print_source_hash:
+        print(source_hash())
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build measures one MI355X only (every SelKV step is independent per layer and "
@@ -301,16 +313,17 @@ def main():
         out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
         out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
 
-    decode_src = os.path.join(ROOT, "paper_2607_16213_amd", "csrc", "decode.hip")
-    traffic = read_traffic(decode_src)
-    out["roofline"] = {"kernel": "decode_split_kernel", "bound": "hbm", "achieved": round(decode_gbs, 1),
+    traffic = read_traffic()
+    out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),
                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_gbs / HBM_PEAK_GBS, 4),
                        "traffic": traffic, "alg_bytes_per_launch": per_decode}
 
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        # a plain elementwise kernel that reads 1 GiB and writes 1 GiB, to
+        # scale the hardware byte counters of profiling passes
+        src = torch.ones((1 << 30) // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
 

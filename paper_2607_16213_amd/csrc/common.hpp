@@ -88,6 +88,60 @@ template <> struct Mma<float> {
   }
 };
 
+// A lane's slice of one row when 16 lanes share the row: d/16 elements of T.
+template <typename T, int D>
+struct Slice {
+  static constexpr int kElems = D / 16;
+  static constexpr int kBytes = kElems * (int)sizeof(T);   // 8, 16 or 32
+};
+
+// Raw slice kept in registers until used (no conversion on load).
+template <typename T, int D>
+struct RawSlice {
+  static constexpr int kBytes = Slice<T, D>::kBytes;
+  uint32_t w[kBytes / 4];
+  __device__ __forceinline__ void load(const char* row, int col) {
+    const char* p = row + col * kBytes;
+    if constexpr (kBytes >= 16) {
+#pragma unroll
+      for (int c = 0; c < kBytes / 16; ++c) {
+        const uint4 v = *reinterpret_cast<const uint4*>(p + c * 16);
+        w[4 * c] = v.x; w[4 * c + 1] = v.y; w[4 * c + 2] = v.z; w[4 * c + 3] = v.w;
+      }
+    } else {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+      w[0] = v.x; w[1] = v.y;
+    }
+  }
+  __device__ __forceinline__ void store(char* row, int col) const {
+    char* p = row + col * kBytes;
+    if constexpr (kBytes >= 16) {
+#pragma unroll
+      for (int c = 0; c < kBytes / 16; ++c)
+        *reinterpret_cast<uint4*>(p + c * 16) = make_uint4(w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]);
+    } else {
+      *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+    }
+  }
+  __device__ __forceinline__ float get(int e) const {
+    if constexpr (sizeof(T) == 4) {
+      return __uint_as_float(w[e]);
+    } else {
+      const uint32_t x = w[e >> 1];
+      return __uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
+    }
+  }
+  __device__ __forceinline__ void put(int e, float f) {
+    if constexpr (sizeof(T) == 4) {
+      w[e] = __float_as_uint(f);
+    } else {
+      const uint32_t h = f32_to_bf16(f);
+      uint32_t& x = w[e >> 1];
+      x = (e & 1) ? ((x & 0x0000ffffu) | (h << 16)) : ((x & 0xffff0000u) | h);
+    }
+  }
+};
+
 __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, 64); }
 __device__ __forceinline__ int xor_shfl(int v, int mask) { return __shfl_xor(v, mask, 64); }
 

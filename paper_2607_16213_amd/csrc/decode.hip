@@ -36,12 +36,6 @@ constexpr int kMaxSplit = 1024;
 constexpr int kReduceThreads = 512;
 
 template <typename T, int D>
-struct Slice {
-  static constexpr int kElems = D / 16;
-  static constexpr int kBytes = kElems * (int)sizeof(T);
-};
-
-template <typename T, int D>
 __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[Slice<T, D>::kElems]) {
   constexpr int B = Slice<T, D>::kBytes;
   const char* p = row + col * B;
@@ -60,34 +54,6 @@ __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[
     x[3] = __uint_as_float(v.y & 0xffff0000u);
   }
 }
-
-// Raw lane slice (d/16 elements, 8/16/32 bytes) kept in registers until used.
-template <typename T, int D>
-struct RawSlice {
-  static constexpr int kBytes = Slice<T, D>::kBytes;
-  uint32_t w[kBytes / 4];
-  __device__ __forceinline__ void load(const char* row, int col) {
-    const char* p = row + col * kBytes;
-    if constexpr (kBytes >= 16) {
-#pragma unroll
-      for (int c = 0; c < kBytes / 16; ++c) {
-        const uint4 v = *reinterpret_cast<const uint4*>(p + c * 16);
-        w[4 * c] = v.x; w[4 * c + 1] = v.y; w[4 * c + 2] = v.z; w[4 * c + 3] = v.w;
-      }
-    } else {
-      const uint2 v = *reinterpret_cast<const uint2*>(p);
-      w[0] = v.x; w[1] = v.y;
-    }
-  }
-  __device__ __forceinline__ float get(int e) const {
-    if constexpr (sizeof(T) == 4) {
-      return __uint_as_float(w[e]);
-    } else {
-      const uint32_t x = w[e >> 1];
-      return __uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
-    }
-  }
-};
 
 // Loads of one step: kUnroll entries per lane group, K and V slices and the bias.
 template <typename T, int D, bool BIAS>

@@ -23,14 +23,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / 64;
 
-// Lane slice of one row: d/16 elements of type T.
-template <typename T, int D>
-struct Slice {
-  static constexpr int kElems = D / 16;
-  static constexpr int kBytes = kElems * (int)sizeof(T);   // 8, 16 or 32
-  static constexpr int kChunks = kBytes >= 16 ? kBytes / 16 : 1;
-};
-
 template <typename T, int D>
 __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[Slice<T, D>::kElems]) {
   constexpr int E = Slice<T, D>::kElems;
@@ -50,37 +42,6 @@ __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[
     x[2] = __uint_as_float(v.y << 16);
     x[3] = __uint_as_float(v.y & 0xffff0000u);
     static_assert(E == 4, "8-byte slices hold four bf16");
-  }
-}
-
-template <typename T, int D>
-__device__ __forceinline__ void copy_slice(char* dst, const char* src, int col) {
-  constexpr int B = Slice<T, D>::kBytes;
-  if constexpr (B >= 16) {
-#pragma unroll
-    for (int c = 0; c < B / 16; ++c) store16(dst + col * B + c * 16, load16(src + col * B + c * 16));
-  } else {
-    *reinterpret_cast<uint2*>(dst + col * B) = *reinterpret_cast<const uint2*>(src + col * B);
-  }
-}
-
-template <typename T, int D>
-__device__ __forceinline__ void store_slice(char* row, int col, const float (&x)[Slice<T, D>::kElems]) {
-  constexpr int B = Slice<T, D>::kBytes;
-  char* p = row + col * B;
-  if constexpr (B >= 16) {
-#pragma unroll
-    for (int c = 0; c < B / 16; ++c) {
-      Chunk16 ch = zero16();
-#pragma unroll
-      for (int e = 0; e < Elem<T>::kPerChunk; ++e) Elem<T>::put(ch, e, x[c * Elem<T>::kPerChunk + e]);
-      store16(p + c * 16, ch);
-    }
-  } else {
-    uint2 v;
-    v.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-    v.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-    *reinterpret_cast<uint2*>(p) = v;
   }
 }
 
@@ -187,42 +148,49 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   float wsum = 0.f;
-#pragma unroll 2
-  for (int ib = 0; ib < ne; ib += 4) {     // uniform trip count; lane group q takes entry ib + q
-    const int i = ib + grp;
-    const bool valid = i < ne;
-    const int src = valid ? i : 0;
-    const int j = __shfl(pos_e, src, 64);
-    const float aj = __shfl(a_e, src, 64);
-    const float vnj = __shfl(vn_e, src, 64);
-    float vj[E];
-    if (valid) {
-      load_slice<T, D>(Vh + (size_t)j * RB, col, vj);
-    } else {
+  // evicted rows, kBatch per lane group with their loads issued together;
+  // lane group q takes entries 4u + q (uniform trip count, masked)
+  constexpr int kBatch = 4;
+  for (int ib0 = 0; ib0 < ne; ib0 += 4 * kBatch) {
+    int jj[kBatch];
+    float ajv[kBatch], vnjv[kBatch];
+    RawSlice<T, D> vr[kBatch];
 #pragma unroll
-      for (int e = 0; e < E; ++e) vj[e] = 0.f;
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = ib0 + 4 * u + grp;
+      const int src = i < ne ? i : 0;
+      jj[u] = __shfl(pos_e, src, 64);
+      ajv[u] = __shfl(a_e, src, 64);
+      vnjv[u] = __shfl(vn_e, src, 64);
     }
-    float dot = 0.f;
 #pragma unroll
-    for (int e = 0; e < E; ++e) dot = fmaf(vj[e], vt[e], dot);
-    dot = sum16(dot);
-    float g = 0.f;
-    if (tslot >= 0) {
-      if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
-        g = 1.f;
-      } else if (a.gate_mode == SELKV_GATE_COSINE) {
-        const float sim = (vnj > 0.f && vn_t > 0.f) ? dot / (vnj * vn_t) : 0.f;
-        g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
+    for (int u = 0; u < kBatch; ++u) vr[u].load(Vh + (size_t)jj[u] * RB, col);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = ib0 + 4 * u + grp;
+      const bool valid = i < ne;
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
+      dot = sum16(dot);
+      float g = 0.f;
+      if (tslot >= 0) {
+        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
+          g = 1.f;
+        } else if (a.gate_mode == SELKV_GATE_COSINE) {
+          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
+          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
+        }
       }
-    }
-    if (valid) {
-      const float w = g * aj;
+      if (valid) {
+        const float w = g * ajv[u];
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vj[e], acc[e]);
-      wsum += w;
-      if (col == 0) {
-        th[e0 + i] = tslot;
-        gh[e0 + i] = g;
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
+        wsum += w;
+        if (col == 0) {
+          th[e0 + i] = tslot;
+          gh[e0 + i] = g;
+        }
       }
     }
   }
@@ -235,21 +203,32 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   wsum += xor_shfl(wsum, 16);
   wsum += xor_shfl(wsum, 32);
 
-  // write the bucket's kept rows: keys gathered, values copied or merged
-  for (int kb = 0; kb < nk; kb += 4) {
-    const int i = kb + grp;
-    const int pos = __shfl(pos_k, i < nk ? i : 0, 64);
-    if (i < nk) {
-      const int k = k0 + i;
-      copy_slice<T, D>(Ko + (size_t)k * RB, Kh + (size_t)pos * RB, col);
-      if (k == tslot && wsum > 0.f) {
-        const float den = a_t + wsum;
-        float out[E];
+  // write the bucket's kept rows: keys gathered, values copied or merged;
+  // kBatch rows per lane group loaded before any is stored
+  for (int kb0 = 0; kb0 < nk; kb0 += 4 * kBatch) {
+    RawSlice<T, D> kr[kBatch], vr[kBatch];
 #pragma unroll
-        for (int e = 0; e < E; ++e) out[e] = fmaf(a_t, vt[e], acc[e]) / den;
-        store_slice<T, D>(Vo + (size_t)k * RB, col, out);
-      } else {
-        copy_slice<T, D>(Vo + (size_t)k * RB, Vh + (size_t)pos * RB, col);
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = kb0 + 4 * u + grp;
+      const int pos = __shfl(pos_k, i < nk ? i : 0, 64);
+      kr[u].load(Kh + (size_t)pos * RB, col);
+      vr[u].load(Vh + (size_t)pos * RB, col);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = kb0 + 4 * u + grp;
+      if (i < nk) {
+        const int k = k0 + i;
+        kr[u].store(Ko + (size_t)k * RB, col);
+        if (k == tslot && wsum > 0.f) {
+          const float den = a_t + wsum;
+          RawSlice<T, D> mv;
+#pragma unroll
+          for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_t, vt[e], acc[e]) / den);
+          mv.store(Vo + (size_t)k * RB, col);
+        } else {
+          vr[u].store(Vo + (size_t)k * RB, col);
+        }
       }
     }
   }
@@ -267,14 +246,21 @@ struct BiasArgs {
   float alpha;
 };
 
-// One wave per bucket.  Lane e loads the bucket's e-th evicted entry and its
-// contribution g * a (all loads in parallel); lane i then owns kept slot
-// k0 + i and adds, in ascending evicted order, the contributions routed to it.
+// One wave per kBiasBuckets consecutive buckets.  For each bucket lane e
+// loads the e-th evicted entry and its contribution g * a, lane i the i-th
+// kept slot; the loads of all the wave's buckets are issued level by level
+// (offsets, then indices / targets / gates, then attention masses).  Lane i
+// then adds the contributions routed to its slot (one wave sum when, as
+// bucket routing guarantees, all routed tokens of the bucket share a target;
+// otherwise in ascending evicted order): R = 1 + absorbed / a_i,
+// bias = alpha * ln R (exactly 0 if nothing was absorbed).
+constexpr int kBiasBuckets = 4;
+
 __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   const int64_t head = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int bucket = blockIdx.x * kWavesPerBlock + wave;
-  if (bucket >= a.nb) return;
+  const int b0 = (blockIdx.x * kWavesPerBlock + wave) * kBiasBuckets;
+  if (b0 >= a.nb) return;
   const int n = a.n, m = a.m;
   const int32_t* kh = a.kept + (size_t)head * m;
   const int32_t* eh = a.evicted + (size_t)head * (n - m);
@@ -282,27 +268,62 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   const float* gh = a.gate + (size_t)head * (n - m);
   const int32_t* oh = a.offs + (size_t)head * (a.nb + 1);
   const float* ah = a.attn + (size_t)head * n;
-  const int start = bucket * a.B;
-  const int end = min(n, start + a.B);
-  const int k0 = oh[bucket], k1 = oh[bucket + 1];
-  const int e0 = start - k0, e1 = end - k1;
-  if (k0 > k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // inconsistent kept list
-  const int ne = e1 - e0;
-  int t_e = -1;
-  float c_e = 0.f;
-  if (lane < ne) {
-    t_e = th[e0 + lane];
-    c_e = gh[e0 + lane] * ah[eh[e0 + lane]];
+
+  const int offv = oh[min(b0 + lane, a.nb)];
+  int k0[kBiasBuckets], k1[kBiasBuckets], e0[kBiasBuckets], ne[kBiasBuckets];
+  bool ok[kBiasBuckets];
+#pragma unroll
+  for (int bi = 0; bi < kBiasBuckets; ++bi) {
+    const int bucket = b0 + bi;
+    k0[bi] = __shfl(offv, bi, 64);
+    k1[bi] = __shfl(offv, bi + 1, 64);
+    const int start = bucket * a.B;
+    const int end = min(n, start + a.B);
+    e0[bi] = start - k0[bi];
+    const int e1 = end - k1[bi];
+    ne[bi] = e1 - e0[bi];
+    ok[bi] = bucket < a.nb && k0[bi] <= k1[bi] && k1[bi] <= m && e0[bi] >= 0 && e0[bi] <= e1 && e1 <= n - m;
   }
-  const int k = k0 + lane;
-  const float ai = lane < k1 - k0 ? ah[kh[k]] : 1.f;
-  float absorbed = 0.f;
-  for (int i = 0; i < ne; ++i) {
-    const int t = __shfl(t_e, i, 64);
-    const float c = __shfl(c_e, i, 64);
-    if (t == k) absorbed += c;
+  int t_e[kBiasBuckets], j_e[kBiasBuckets], pos_k[kBiasBuckets];
+  float g_e[kBiasBuckets];
+#pragma unroll
+  for (int bi = 0; bi < kBiasBuckets; ++bi) {
+    const bool has_e = ok[bi] && lane < ne[bi];
+    const bool has_k = ok[bi] && lane < k1[bi] - k0[bi];
+    t_e[bi] = has_e ? th[e0[bi] + lane] : -1;
+    g_e[bi] = has_e ? gh[e0[bi] + lane] : 0.f;
+    j_e[bi] = has_e ? eh[e0[bi] + lane] : 0;
+    pos_k[bi] = has_k ? kh[k0[bi] + lane] : 0;
   }
-  if (k < k1) a.bias[(size_t)head * m + k] = absorbed > 0.f ? a.alpha * log1pf(absorbed / ai) : 0.f;
+  float c_e[kBiasBuckets], a_k[kBiasBuckets];
+#pragma unroll
+  for (int bi = 0; bi < kBiasBuckets; ++bi) {
+    c_e[bi] = g_e[bi] * ah[j_e[bi]];
+    a_k[bi] = ah[pos_k[bi]];
+  }
+#pragma unroll
+  for (int bi = 0; bi < kBiasBuckets; ++bi) {
+    if (!ok[bi]) continue;                       // wave-uniform
+    const int k = k0[bi] + lane;
+    float absorbed = 0.f;
+    // bucket routing sends every routed token of a bucket to one slot: then
+    // one wave sum does; otherwise add per slot in ascending evicted order
+    const int t0 = __shfl(t_e[bi], 0, 64);
+    const bool same = __ballot(lane >= ne[bi] || t_e[bi] == t0) == ~0ull;
+    if (same) {
+      float tot = c_e[bi];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
+      absorbed = (k == t0) ? tot : 0.f;
+    } else {
+      for (int i = 0; i < ne[bi]; ++i) {
+        const int t = __shfl(t_e[bi], i, 64);
+        const float c = __shfl(c_e[bi], i, 64);
+        if (t == k) absorbed += c;
+      }
+    }
+    if (k < k1[bi]) a.bias[(size_t)head * m + k] = absorbed > 0.f ? a.alpha * log1pf(absorbed / a_k[bi]) : 0.f;
+  }
 }
 
 }  // namespace
@@ -371,7 +392,8 @@ hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const flo
   a.nb = s.nb;
   a.B = bucket;
   a.alpha = alpha;
-  const dim3 grid((s.nb + kWavesPerBlock - 1) / kWavesPerBlock, (unsigned)s.heads);
+  const int per_block = kWavesPerBlock * kBiasBuckets;
+  const dim3 grid((s.nb + per_block - 1) / per_block, (unsigned)s.heads);
   hipLaunchKernelGGL(bias_bucket_kernel, grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }

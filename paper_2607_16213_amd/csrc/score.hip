@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   const int full_end = min(ke, n - W + 1);
 
   __shared__ float colacc[RW][kMaxChunkKeys];
-  __shared__ float vn_l[kMaxChunkKeys];
+  __shared__ float vn_l[RW][kMaxChunkKeys];   // squared-norm partials, one per row half
 
   for (int rg = 0; rg < a.nrg; ++rg) {
     const int row0 = rg * ROWS + half * NRB * 16;
@@ -244,15 +244,22 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
         iL[rb][i] = v.y;           // 0 for padding rows
         wi[rb][i] = row < a.R ? row % W : -1;
       }
-    const bool norms = rg == 0 && half == 0;   // one wave per tile reads V once
+    // each row half reads its share of every V row once: chunks c with c % RW == half
+    const bool norms = rg == 0;
 
     int t = kb + stream * 16;
     Chunk16 kcur[NCH], knxt[NCH];
     if (t < ke) load_tile<T, D>(Kh, t, ke - 1, col, grp, kcur);
     for (; t < ke; t += TS * 16) {
       load_tile<T, D>(Kh, t + TS * 16, ke - 1, col, grp, knxt);
-      Chunk16 vf[NCH];
-      if (norms) load_tile<T, D>(Vh, t, ke - 1, col, grp, vf);
+      constexpr int NV = NCH / RW > 0 ? NCH / RW : 1;
+      Chunk16 vf[NV];
+      if (norms) {
+        const int vkey = min(t + col, ke - 1);
+#pragma unroll
+        for (int c = 0; c < NV; ++c)
+          vf[c] = load16(Vh + (size_t)vkey * Row<T, D>::kBytes + ((c * RW + half) * 4 + grp) * 16);
+      }
       const bool fast = t + 16 <= full_end;
       const int key = t + col;
       float cs = 0.f;
@@ -275,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
       if (norms) {
         float ss = 0.f;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c)
+        for (int c = 0; c < NV; ++c)
 #pragma unroll
           for (int e = 0; e < EPC; ++e) {
             const float x = Elem<T>::get(vf[c], e);
@@ -283,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
           }
         ss += xor_shfl(ss, 16);
         ss += xor_shfl(ss, 32);
-        if (grp == 0 && key < ke) vn_l[local] = sqrtf(ss);
+        if (grp == 0 && key < ke) vn_l[half][local] = ss;
       }
 #pragma unroll
       for (int c = 0; c < NCH; ++c) kcur[c] = knxt[c];
@@ -296,7 +303,10 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
 #pragma unroll
     for (int h = 1; h < RW; ++h) total += colacc[h][local];
     const float av = total / (float)a.G;
-    const float vn = vn_l[local];
+    float ss = vn_l[0][local];
+#pragma unroll
+    for (int h = 1; h < RW; ++h) ss += vn_l[h][local];
+    const float vn = sqrtf(ss);
     const size_t o = (size_t)head * n + k;
     a.attn[o] = av;
     a.vnorm[o] = vn;
@@ -315,7 +325,8 @@ __global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* cbuf,
   float s = 0.f;
   for (int t = -h; t <= h; ++t) {
     const int jj = j + t;
-    if (jj >= 0 && jj < n_cand) s += c[jj];
+    const float v = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
+    s += (jj >= 0 && jj < n_cand) ? v : 0.f;
   }
   score[(size_t)head * n_cand + j] = s / (float)K;
 }
