@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
 METRIC = "SelKV compress tokens/s @32k,100k; biased-decode step µs; % HBM/MFMA peak"
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_ctx100k_pmc.txt")
 
@@ -42,6 +43,8 @@ def parse():
     ap.add_argument("--cpu-heads", type=int, default=6, help="(layer, head) slices the oracle compresses")
     ap.add_argument("--no-graph", action="store_true", help="launch decode eagerly instead of from a HIP graph")
     ap.add_argument("--print-source-hash", action="store_true", help="print the decode source hash and exit")
+    ap.add_argument("--full-cosine-layers", type=int, default=1,
+                    help="layers timed with the all-pairs cosine routing variant (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
     return ap.parse_args()
@@ -250,6 +253,43 @@ def measure(job, steps, warmup):
     return wall, st
 
 
+def measure_full_cosine(job, layers, reps=3):
+    """The all-pairs cosine routing variant of the merge call on the first
+    `layers` layers of the resident workload, fed the compressed job's own
+    attn / vnorm / kept / evicted.  The contraction is 2 * (n - m) * m * d
+    flops per KV head; its peak is the dense bf16 (or fp32) MFMA rate."""
+    torch, selkv, w = job.torch, job.selkv, job.w
+    B, H, d, n, m = w.batch, w.n_heads_kv, w.head_dim, w.seq_len, job.m
+    LB = layers * B
+    p = selkv.params(batch=LB, n_heads_kv=H, group=w.group, head_dim=d, seq_len=n, window=w.window,
+                     kv_dtype=w.dtype, budget_ratio=w.budgets[0], route_mode="full_cosine")
+    dev = job.K.device
+    c = job.comp
+    K_out = torch.empty((LB, H, m, d), dtype=job.K.dtype, device=dev)
+    V_out = torch.empty_like(K_out)
+    target = torch.empty((LB, H, n - m), dtype=torch.int32, device=dev)
+    gate = torch.empty((LB, H, n - m), dtype=torch.float32, device=dev)
+    ws = selkv.workspace(p, selkv.CALL_MERGE, dev)
+    sl = slice(0, LB)
+    args = (p, job.Kf[sl], job.Vf[sl], c.attn[sl], c.vnorm[sl], c.kept[sl], c.evicted[sl], K_out, V_out, target, gate,
+            ws)
+    selkv.merge(*args)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        selkv.merge(*args)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    flops = 2.0 * (n - m) * m * d * LB * H
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"layers": layers, "merge_ms": round(ms, 4), "flops": flops, "achieved_TFLOPs": round(tf, 1),
+            "peak_TFLOPs": peak, "frac_mfma": round(tf / peak, 4),
+            "note": "time of the whole merge call (contraction + grouping + segmented merge)"}
+
+
 def main():
     args = parse()
     if args.print_source_hash:
@@ -312,6 +352,9 @@ def main():
         out["full_cache_decode_us_per_layer_step"] = round(full_us, 3)
         out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
         out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
+
+    if args.full_cosine_layers > 0:
+        out["full_cosine_routing"] = measure_full_cosine(job, min(args.full_cosine_layers, w.layers))
 
     traffic = read_traffic()
     out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),

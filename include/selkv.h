@@ -166,7 +166,9 @@ SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, i
  * BUCKET routing: evicted token j goes to the kept token of its bucket
  * floor(j/B) with the largest attn (lowest position on ties), or nowhere
  * (-1, dropped) if the bucket keeps no token.  FULL_COSINE routing: to the
- * kept token with the most cosine-similar value (lowest slot on ties).
+ * kept token with the most cosine-similar value (lowest slot on ties),
+ * found by an all-pairs MFMA contraction per KV head; the tokens routed to
+ * each slot are then merged in ascending order.
  * Gate: sim = v_j . v_t / (||v_j|| ||v_t||) against the pre-merge target
  * value (0 if a norm is 0), g = clamp((sim - tau)/T, 0, 1) in COSINE mode,
  * 0 in DROP, 1 in MERGE_ALL; unrouted tokens get g = 0.
@@ -192,7 +194,8 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
  * was absorbed.
  * In:  attn [B, H_kv, n]; kept_idx, evicted_idx; target, gate (from
  *      selkv_merge with the same params: under BUCKET routing every routed
- *      token lies in its target's bucket, which this call relies on).
+ *      token lies in its target's bucket, which this call relies on; under
+ *      FULL_COSINE any target slot is allowed).
  * Out: bias [B, H_kv, m] fp32.
  * Workspace: selkv_workspace_size(p, SELKV_CALL_BIAS, 0). */
 SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,

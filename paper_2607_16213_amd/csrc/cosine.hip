@@ -1,0 +1,455 @@
+// Full-cosine routing (the all-pairs alternative of Sec. 3.4) for
+// selkv_merge / selkv_bias with SELKV_ROUTE_FULL_COSINE.
+//
+//   match    per KV head an |E| x |S| x d bf16 (or fp32) MFMA contraction of
+//            the evicted value rows against the kept value rows, with the
+//            epilogue fused: cos = dot / (||v_j|| ||v_i||) from the fp32 norms,
+//            running argmax per evicted row (lowest kept slot on ties), then
+//            the gate of Sec. 3.5 from the best cosine.  The |E| x |S| matrix
+//            is never written.
+//   group    a stable grouping of the evicted tokens by target slot:
+//            integer-atomic counts, an exclusive scan, and one wave per head
+//            scattering the tokens in ascending order (ranks among equal
+//            targets from ballots), so every slot's list is ascending.
+//   merge    one wave per kept slot: Eq. 5 over its list in a fixed order;
+//            keys gathered, values copied bit for bit when nothing is absorbed.
+//   bias     one wave per kept slot: Eq. 6 over the same lists.
+// All results are independent of scheduling.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace selkv {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kMatchRowBlocks = 4;   // 16-row MFMA blocks of evicted rows per wave
+
+template <typename T, int D>
+struct Row {
+  static constexpr int kBytes = D * (int)sizeof(T);
+  static constexpr int kNch = kBytes / 64;
+};
+
+struct MatchArgs {
+  const char* V;
+  const float* vnorm;
+  const int32_t* kept;
+  const int32_t* evicted;
+  int32_t* target;
+  float* gate;
+  int n, m, gate_mode;
+  float tau, inv_temp;
+};
+
+// Evicted rows r0 .. r0+63 of one head against every kept row.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
+  constexpr int NCH = Row<T, D>::kNch;
+  constexpr int RB = Row<T, D>::kBytes;
+  constexpr int NRB = kMatchRowBlocks;
+  const int64_t head = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int n = a.n, m = a.m, ne = n - m;
+  const int r0 = (blockIdx.x * kWaves + wave) * NRB * 16;
+  if (r0 >= ne) return;   // whole wave; no barrier below
+  const char* Vh = a.V + (size_t)head * n * RB;
+  const float* vnh = a.vnorm + (size_t)head * n;
+  const int32_t* kh = a.kept + (size_t)head * m;
+  const int32_t* eh = a.evicted + (size_t)head * ne;
+
+  // A operand: evicted value rows (lane row = col), chunks 4c + grp
+  Chunk16 q[NRB][NCH];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    const int e = min(r0 + rb * 16 + col, ne - 1);
+    const int pos = eh[e];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) q[rb][c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
+  }
+  // inverse norms of the output rows of this lane (rows 4*grp + i of each block)
+  float inv_j[NRB][4], best[NRB][4];
+  int bidx[NRB][4];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = min(r0 + rb * 16 + grp * 4 + i, ne - 1);
+      const float vn = vnh[eh[e]];
+      inv_j[rb][i] = vn > 0.f ? 1.f / vn : 0.f;
+      best[rb][i] = kNegInf;
+      bidx[rb][i] = 0;
+    }
+
+  // kept tiles of 16 rows; the next tile's loads are issued before this one is used
+  Chunk16 kcur[NCH], knxt[NCH];
+  float icur, inxt;
+  {
+    const int pos = kh[min(col, m - 1)];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) kcur[c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
+    const float vn = vnh[pos];
+    icur = vn > 0.f ? 1.f / vn : 0.f;
+  }
+  for (int t = 0; t < m; t += 16) {
+    {
+      const int pos = kh[min(t + 16 + col, m - 1)];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) knxt[c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
+      const float vn = vnh[pos];
+      inxt = vn > 0.f ? 1.f / vn : 0.f;
+    }
+    const int slot = t + col;
+    const bool valid = slot < m;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) acc = Mma<T>::step(q[rb][c], kcur[c], acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = acc[i] * icur * inv_j[rb][i];
+        if (valid && v > best[rb][i]) {   // slots rise along the lane: ties keep the lower slot
+          best[rb][i] = v;
+          bidx[rb][i] = slot;
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) kcur[c] = knxt[c];
+    icur = inxt;
+  }
+
+  // merge the 16 lanes (slot subsets) of each row: larger cosine, then lower slot
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        const float ob = xor_shfl(best[rb][i], off);
+        const int oi = xor_shfl(bidx[rb][i], off);
+        if (ob > best[rb][i] || (ob == best[rb][i] && oi < bidx[rb][i])) {
+          best[rb][i] = ob;
+          bidx[rb][i] = oi;
+        }
+      }
+  if (col == 0) {
+    int32_t* th = a.target + (size_t)head * ne;
+    float* gh = a.gate + (size_t)head * ne;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = r0 + rb * 16 + grp * 4 + i;
+        if (e < ne) {
+          float g;
+          if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
+          else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
+          else g = fminf(1.f, fmaxf(0.f, (best[rb][i] - a.tau) * a.inv_temp));
+          th[e] = bidx[rb][i];
+          gh[e] = g;
+        }
+      }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void fill_zero_kernel(int32_t* p, int64_t count) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < count) p[i] = 0;
+}
+
+// cnt[head][t] += 1 for every routed evicted token (integer atomics).
+__global__ __launch_bounds__(kThreads) void group_count_kernel(const int32_t* target, int32_t* cnt, int ne, int m) {
+  const int64_t head = blockIdx.y;
+  const int e = blockIdx.x * kThreads + threadIdx.x;
+  if (e >= ne) return;
+  const int t = target[(size_t)head * ne + e];
+  if (t >= 0 && t < m) atomicAdd(cnt + (size_t)head * (m + 1) + t, 1);
+}
+
+// In place: cnt[head][0..m] becomes the exclusive prefix sum (off[m] = total).
+__global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
+  const int64_t head = blockIdx.x;
+  int32_t* c = cnt + (size_t)head * (m + 1);
+  __shared__ int s_w[16];
+  __shared__ int s_run;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) s_run = 0;
+  __syncthreads();
+  for (int base = 0; base <= m; base += 1024) {
+    const int i = base + tid;
+    const int v = (i < m) ? c[i] : 0;
+    const int incl = wave_inclusive_scan(v, lane);
+    if (lane == 63) s_w[wave] = incl;
+    __syncthreads();
+    int woff = 0;
+    for (int w = 0; w < wave; ++w) woff += s_w[w];
+    int total = 0;
+    for (int w = 0; w < 16; ++w) total += s_w[w];
+    const int run = s_run;
+    if (i <= m) c[i] = run + woff + incl - v;
+    __syncthreads();
+    if (tid == 0) s_run = run + total;
+    __syncthreads();
+  }
+}
+
+// One wave per head: evicted tokens in ascending order, 64 at a time; each
+// token's rank among equal targets in its group of 64 comes from ballots.
+// The write cursors live in LDS; slots are swept in ranges of kCursorSlots.
+constexpr int kCursorSlots = 16384;
+
+__global__ __launch_bounds__(64) void group_scatter_kernel(const int32_t* target, const int32_t* off, int32_t* list,
+                                                           int ne, int m) {
+  __shared__ int32_t cur[kCursorSlots];
+  const int64_t head = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int32_t* th = target + (size_t)head * ne;
+  const int32_t* oh = off + (size_t)head * (m + 1);
+  int32_t* lh = list + (size_t)head * ne;
+  int nbits = 1;
+  while ((1 << nbits) < kCursorSlots) ++nbits;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int s0 = 0; s0 < m; s0 += kCursorSlots) {
+    const int range = min(kCursorSlots, m - s0);
+    for (int s = lane; s < range; s += 64) cur[s] = oh[s0 + s];
+    __syncthreads();
+    for (int base = 0; base < ne; base += 64) {
+      const int e = base + lane;
+      const int t = (e < ne ? th[e] : -1) - s0;       // slot relative to the range
+      const bool valid = t >= 0 && t < range;
+      uint64_t peers = __ballot(valid);
+      for (int b = 0; b < nbits; ++b) {                 // lanes with the same slot
+        const bool bit = (t >> b) & 1;
+        const uint64_t ones = __ballot(valid && bit);
+        peers &= bit ? ones : ~ones;
+      }
+      if (!valid) peers = 0ull;
+      const int rank = __popcll(peers & below);
+      const int start = valid ? cur[t] : 0;
+      if (valid) lh[start + rank] = e;
+      const bool last = valid && ((peers >> lane) >> 1) == 0ull;   // highest lane of its slot
+      __syncthreads();   // every peer has read the cursor
+      if (last) cur[t] = start + rank + 1;
+      __syncthreads();
+    }
+  }
+}
+
+struct GroupMergeArgs {
+  const char* K;
+  const char* V;
+  const float* attn;
+  const int32_t* kept;
+  const int32_t* evicted;
+  const float* gate;
+  const int32_t* off;
+  const int32_t* list;
+  char* K_out;
+  char* V_out;
+  float* bias;
+  int n, m;
+  float alpha;
+};
+
+// One wave per kept slot: Eq. 5 (and the Eq. 6 bias when `bias` is set) over
+// the slot's ascending list; lane group q takes list entries q, q+4, ...
+template <typename T, int D, bool VALUES>
+__global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a) {
+  constexpr int E = Slice<T, D>::kElems;
+  constexpr int RB = D * (int)sizeof(T);
+  const int64_t head = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int s = blockIdx.x * kWaves + wave;
+  const int n = a.n, m = a.m, ne = n - m;
+  if (s >= m) return;
+  const int32_t* kh = a.kept + (size_t)head * m;
+  const int32_t* eh = a.evicted + (size_t)head * ne;
+  const float* gh = a.gate + (size_t)head * ne;
+  const int32_t* oh = a.off + (size_t)head * (m + 1);
+  const int32_t* lh = a.list + (size_t)head * ne;
+  const float* ah = a.attn + (size_t)head * n;
+  const int pos = kh[s];
+  const int l0 = oh[s], l1 = oh[s + 1];
+  const float a_s = ah[pos];
+
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  float wsum = 0.f;
+  for (int lb = l0; lb < l1; lb += 64) {
+    // lane-parallel metadata of up to 64 list entries
+    const int li = lb + lane;
+    int jp = 0;
+    float w = 0.f;
+    if (li < l1) {
+      const int e = lh[li];
+      jp = eh[e];
+      w = gh[e] * ah[jp];
+    }
+    const int cnt = min(64, l1 - lb);
+    if (!VALUES) {
+      float t = w;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) t += xor_shfl(t, o);
+      wsum += t;
+      continue;
+    }
+    constexpr int kBatch = 4;
+    for (int ib0 = 0; ib0 < cnt; ib0 += 4 * kBatch) {
+      int jj[kBatch];
+      float wv[kBatch];
+      RawSlice<T, D> vr[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        const int src = i < cnt ? i : 0;
+        // both shuffles run on every lane: a shuffle under a lane-dependent
+        // condition would read inactive source lanes
+        jj[u] = __shfl(jp, src, 64);
+        wv[u] = __shfl(w, src, 64);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) vr[u].load(a.V + ((size_t)head * n + jj[u]) * RB, col);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        if (i < cnt) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] = fmaf(wv[u], vr[u].get(e), acc[e]);
+          wsum += wv[u];
+        }
+      }
+    }
+  }
+  if (!VALUES) {
+    if (lane == 0) a.bias[(size_t)head * m + s] = wsum > 0.f ? a.alpha * log1pf(wsum / a_s) : 0.f;
+    return;
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    acc[e] += xor_shfl(acc[e], 16);
+    acc[e] += xor_shfl(acc[e], 32);
+  }
+  wsum += xor_shfl(wsum, 16);
+  wsum += xor_shfl(wsum, 32);
+  if (grp == 0) {
+    const char* krow = a.K + ((size_t)head * n + pos) * RB;
+    const char* vrow = a.V + ((size_t)head * n + pos) * RB;
+    RawSlice<T, D> kr, vr;
+    kr.load(krow, col);
+    vr.load(vrow, col);
+    kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
+    if (wsum > 0.f) {
+      const float den = a_s + wsum;
+      RawSlice<T, D> mv;
+#pragma unroll
+      for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_s, vr.get(e), acc[e]) / den);
+      mv.store(a.V_out + ((size_t)head * m + s) * RB, col);
+    } else {
+      vr.store(a.V_out + ((size_t)head * m + s) * RB, col);
+    }
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+GroupPlan plan_group(const Shape& s) {
+  GroupPlan p{};
+  const size_t ne = (size_t)(s.n - s.m);
+  p.off_off = 0;
+  p.cursor_off = align256((size_t)s.heads * (s.m + 1) * sizeof(int32_t));
+  p.list_off = p.cursor_off;
+  p.bytes = p.list_off + align256((ne > 0 ? ne : 1) * (size_t)s.heads * sizeof(int32_t));
+  return p;
+}
+
+hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
+                               const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
+                               float* gate, hipStream_t st) {
+  const int ne = s.n - s.m;
+  if (ne <= 0) return hipSuccess;
+  MatchArgs a{};
+  a.V = static_cast<const char*>(V);
+  a.vnorm = vnorm;
+  a.kept = kept;
+  a.evicted = evicted;
+  a.target = target;
+  a.gate = gate;
+  a.n = s.n;
+  a.m = s.m;
+  a.gate_mode = gate_mode;
+  a.tau = tau;
+  a.inv_temp = 1.f / temp;
+  const int rows_per_block = kWaves * kMatchRowBlocks * 16;
+  const dim3 grid((ne + rows_per_block - 1) / rows_per_block, (unsigned)s.heads);
+  if (dtype == SELKV_BF16) {
+    if (s.d == 128) hipLaunchKernelGGL((cosine_match_kernel<bf16_t, 128>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((cosine_match_kernel<bf16_t, 64>), grid, dim3(kThreads), 0, st, a);
+  } else {
+    if (s.d == 128) hipLaunchKernelGGL((cosine_match_kernel<float, 128>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((cosine_match_kernel<float, 64>), grid, dim3(kThreads), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st) {
+  const int ne = s.n - s.m;
+  char* w = static_cast<char*>(ws);
+  int32_t* off = reinterpret_cast<int32_t*>(w + p.off_off);
+  int32_t* list = reinterpret_cast<int32_t*>(w + p.list_off);
+  const int64_t cnt = s.heads * (int64_t)(s.m + 1);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((cnt + kThreads - 1) / kThreads)), dim3(kThreads), 0, st, off,
+                     cnt);
+  if (ne > 0)
+    hipLaunchKernelGGL(group_count_kernel, dim3((ne + kThreads - 1) / kThreads, (unsigned)s.heads), dim3(kThreads), 0,
+                       st, target, off, ne, s.m);
+  hipLaunchKernelGGL(group_scan_kernel, dim3((unsigned)s.heads), dim3(1024), 0, st, off, s.m);
+  if (ne > 0)
+    hipLaunchKernelGGL(group_scatter_kernel, dim3((unsigned)s.heads), dim3(64), 0, st, target, off, list, ne, s.m);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
+                              const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
+                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, hipStream_t st) {
+  const char* w = static_cast<const char*>(ws);
+  GroupMergeArgs a{};
+  a.K = static_cast<const char*>(K);
+  a.V = static_cast<const char*>(V);
+  a.attn = attn;
+  a.kept = kept;
+  a.evicted = evicted;
+  a.gate = gate;
+  a.off = reinterpret_cast<const int32_t*>(w + p.off_off);
+  a.list = reinterpret_cast<const int32_t*>(w + p.list_off);
+  a.K_out = static_cast<char*>(K_out);
+  a.V_out = static_cast<char*>(V_out);
+  a.bias = bias;
+  a.n = s.n;
+  a.m = s.m;
+  a.alpha = alpha;
+  const dim3 grid((s.m + kWaves - 1) / kWaves, (unsigned)s.heads);
+  const bool values = bias == nullptr;
+#define SELKV_GM(T, D)                                                                        \
+  do {                                                                                        \
+    if (values) hipLaunchKernelGGL((group_merge_kernel<T, D, true>), grid, dim3(kThreads), 0, st, a); \
+    else hipLaunchKernelGGL((group_merge_kernel<T, D, false>), grid, dim3(kThreads), 0, st, a);       \
+  } while (0)
+  if (dtype == SELKV_BF16) {
+    if (s.d == 128) SELKV_GM(bf16_t, 128);
+    else SELKV_GM(bf16_t, 64);
+  } else {
+    if (s.d == 128) SELKV_GM(float, 128);
+    else SELKV_GM(float, 64);
+  }
+#undef SELKV_GM
+  return hipGetLastError();
+}
+
+}  // namespace selkv

@@ -36,7 +36,13 @@ struct DecodePlan {
   size_t bytes;
 };
 
+// Workspace of the grouping by target slot (full-cosine routing).
+struct GroupPlan {
+  size_t off_off, cursor_off, list_off, bytes;
+};
+
 ScorePlan plan_score(const Shape& s, int dtype);
+GroupPlan plan_group(const Shape& s);
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G);
 size_t bucket_offsets_bytes(const Shape& s);
 
@@ -53,6 +59,13 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
                               const float* gate, float* bias, hipStream_t st);
+hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
+                               const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
+                               float* gate, hipStream_t st);
+hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st);
+hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
+                              const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
+                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, hipStream_t st);
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int d, int G, int dtype, float scale,
                          const DecodePlan& plan, const void* q, const void* K, const void* V, const float* bias,
                          float* out, void* ws, hipStream_t st);

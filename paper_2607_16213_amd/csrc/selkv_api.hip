@@ -117,7 +117,9 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
     case SELKV_CALL_SCORE: *bytes = plan_score(s, p->kv_dtype).bytes; return SELKV_OK;
     case SELKV_CALL_SELECT: *bytes = 0; return SELKV_OK;
     case SELKV_CALL_MERGE:
-    case SELKV_CALL_BIAS: *bytes = bucket_offsets_bytes(s); return SELKV_OK;
+    case SELKV_CALL_BIAS:
+      *bytes = p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
+      return SELKV_OK;
     default: return SELKV_EINVAL;
   }
 }
@@ -157,7 +159,6 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
   Shape s;
   selkv_status st = make_shape(p, &s);
   if (st != SELKV_OK) return st;
-  if (p->route_mode != SELKV_ROUTE_BUCKET) return SELKV_EUNSUPPORTED;
   const bool has_ev = s.n > s.m;
   if (!K || !V || !attn || !vnorm || !kept_idx || !K_out || !V_out) return SELKV_EINVAL;
   if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
@@ -165,6 +166,17 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
       !aligned(vnorm, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
       !aligned(gate, 4))
     return SELKV_EALIGN;
+  if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {
+    const GroupPlan gp = plan_group(s);
+    if ((st = check_ws(ws, ws_bytes, gp.bytes)) != SELKV_OK) return st;
+    hipError_t e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm,
+                                       kept_idx, evicted_idx, target, gate, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    e = launch_group(s, gp, target, ws, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out,
+                                         V_out, nullptr, 0.f, stream));
+  }
   const size_t need = bucket_offsets_bytes(s);
   if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
   int32_t* offs = static_cast<int32_t*>(ws);
@@ -181,13 +193,20 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
   Shape s;
   selkv_status st = make_shape(p, &s);
   if (st != SELKV_OK) return st;
-  if (p->route_mode != SELKV_ROUTE_BUCKET) return SELKV_EUNSUPPORTED;
   const bool has_ev = s.n > s.m;
   if (!attn || !kept_idx || !bias) return SELKV_EINVAL;
   if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
   if (!aligned(attn, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
       !aligned(gate, 4) || !aligned(bias, 4))
     return SELKV_EALIGN;
+  if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {
+    const GroupPlan gp = plan_group(s);
+    if ((st = check_ws(ws, ws_bytes, gp.bytes)) != SELKV_OK) return st;
+    hipError_t e = launch_group(s, gp, target, ws, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    return hip_status(launch_group_merge(s, gp, p->kv_dtype, nullptr, nullptr, attn, kept_idx, evicted_idx, gate, ws,
+                                         nullptr, nullptr, bias, p->alpha, stream));
+  }
   const size_t need = bucket_offsets_bytes(s);
   if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
   int32_t* offs = static_cast<int32_t*>(ws);

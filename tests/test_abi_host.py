@@ -121,4 +121,6 @@ def test_call_validation_before_launch(S):
     assert g(ctypes.byref(p), fake, fake, fake, ctypes.c_void_p(0x10001), 64, fake, fake, 1 << 30, None) == 4
     pf = S.params(seq_len=256, route_mode="full_cosine")
     m = S.lib.selkv_merge
-    assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, 1 << 30, None) == 3
+    assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, 16, None) == 5
+    assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, mis, fake, fake, fake, fake, 1 << 30, None) == 4
+    assert S.workspace_bytes(pf, S.CALL_MERGE) > S.workspace_bytes(S.params(seq_len=256), S.CALL_MERGE)

@@ -406,3 +406,112 @@ def test_decode_hip_graph_replays_match_eager(S):
         assert torch.equal(outs, ref), f"replay {rep}"
         dec.run(qs[1], c.K_out, c.V_out, None)       # eager work between replays
         torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ full-cosine routing (all-pairs variant)
+def oracle_fullcos(K64, V64, a32, vn, kept, ev, p, gate_mode):
+    target, best = O.route_full_cosine(V64, kept, ev)
+    g = O.gate(V64, kept, ev, target, gate_mode, float(np.float32(p.gate_threshold)),
+               float(np.float32(p.gate_temperature)))
+    _, v_out, _ = O.merge(K64, V64, a32, kept, ev, target, g)
+    return target, best, g, v_out
+
+
+FULLCOS = [
+    dict(batch=1, H=2, G=2, d=64, n=512, W=32, dtype="fp32"),
+    dict(batch=1, H=2, G=4, d=128, n=1000, W=32, dtype="bf16"),
+    dict(batch=2, H=1, G=3, d=64, n=300, W=16, dtype="bf16", gate_mode=2),
+    dict(batch=1, H=1, G=2, d=128, n=200, W=8, dtype="fp32", gate_mode=1),
+    dict(batch=1, H=2, G=2, d=64, n=700, W=32, dtype="bf16", gate_threshold=0.2, gate_temperature=0.5,
+         budget_ratio=0.1),
+    dict(batch=1, H=1, G=2, d=64, n=300, W=32, dtype="bf16", budget_ratio=1.0),       # nothing evicted
+    dict(batch=1, H=1, G=2, d=64, n=100, W=8, dtype="fp32", budget_ratio=0.05),       # m < 16: one partial tile
+    dict(batch=1, H=1, G=2, d=64, n=20000, W=32, dtype="bf16", budget_ratio=0.9),     # m > 16384 cursor slots
+]
+
+
+@pytest.mark.parametrize("case", FULLCOS, ids=[f"fullcos{i}" for i in range(len(FULLCOS))])
+def test_full_cosine_routing_stagewise(S, case):
+    """a9: the all-pairs cosine routing on MFMA, the stable grouping by
+    target and the segmented merge / bias, each fed the oracle's inputs.
+    Target slots must match except where the two best cosines lie within
+    4e-6 of each other (fp32 accumulation over d <= 128 terms of unit-scale
+    products); such rows are counted and their two candidate slots left out
+    of the value checks."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 7 + 1, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=8, device=DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    V[:, :, 7].zero_()
+    p = make_params(S, case, route_mode="full_cosine", **kw)
+    tol = TOL[case["dtype"]]
+    B, H, n, d = K.shape
+    m, mr, ms = S.budget(p)
+    comp = S.Compressor(p, DEV)
+    S.score(p, K, V, Q, comp.score, comp.attn, comp.vnorm, comp.ws_score)
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(K), np64(V), np64(Q)
+    chains = {}
+    a_in, vn_in = comp.attn.clone(), comp.vnorm.clone()
+    for b in range(B):
+        for h in range(H):
+            ch = oracle_chain(K64[b, h], V64[b, h], Q64[b, h * p.group:(h + 1) * p.group], p, GATE[p.gate_mode])
+            chains[(b, h)] = ch
+            comp.kept[b, h] = torch.as_tensor(ch["kept"], dtype=torch.int32)
+            comp.evicted[b, h] = torch.as_tensor(ch["ev"], dtype=torch.int32)
+            a_in[b, h] = torch.as_tensor(ch["a32"], dtype=torch.float32)
+            vn_in[b, h] = torch.as_tensor(ch["vn"], dtype=torch.float32)
+    S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
+            comp.ws_merge)
+    torch.cuda.synchronize()
+    ties = 0
+    for (b, h), ch in chains.items():
+        target, best, g, v_out = oracle_fullcos(K64[b, h], V64[b, h], ch["a32"], ch["vn"], ch["kept"], ch["ev"], p,
+                                                GATE[p.gate_mode])
+        tg = comp.target[b, h].cpu().numpy()
+        skip = set()
+        vk = V64[b, h][ch["kept"]]
+        nk = np.linalg.norm(vk, axis=1)
+        for e in np.flatnonzero(tg != target):
+            vj = V64[b, h][ch["ev"][e]]
+            nj = np.linalg.norm(vj)
+            cos = lambda s: 0.0 if nk[s] == 0 or nj == 0 else float(vk[s] @ vj) / (nk[s] * nj)
+            assert abs(cos(tg[e]) - cos(target[e])) <= 4e-6, \
+                f"routing differs at evicted {e}: {tg[e]} vs {target[e]}"
+            skip |= {int(tg[e]), int(target[e])}
+            ties += 1
+        keep_e = np.array([int(target[e]) not in skip for e in range(len(target))], dtype=bool)
+        gate_tol = 8e-6 / float(np.float32(p.gate_temperature))     # cosines agree to ~4e-6
+        assert np.abs(np64(comp.gate[b, h])[keep_e] - g[keep_e]).max(initial=0) <= gate_tol
+        assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(ch["kept"])])
+        rows = np.array([s not in skip for s in range(m)], dtype=bool)
+        assert_close_rows(np64(comp.V_out[b, h])[rows], v_out[rows], tol, "V_out")
+        # bias through the same grouping, fed the oracle's targets and gates
+        g32 = g.astype(np.float32).astype(np.float64)
+        comp.target[b, h] = torch.as_tensor(target, dtype=torch.int32)
+        comp.gate[b, h] = torch.as_tensor(g32, dtype=torch.float32)
+        chains[(b, h)]["fc_bias"] = O.ratio_bias(ch["a32"], ch["kept"], ch["ev"], target, g32,
+                                                 float(np.float32(p.alpha)))
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    torch.cuda.synchronize()
+    for (b, h), ch in chains.items():
+        err = np.abs(np64(comp.bias[b, h]) - ch["fc_bias"]).max(initial=0)
+        assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias err {err:.3e}"
+    print(f"full-cosine routing near-ties: {ties}")
+
+
+def test_full_cosine_deterministic_and_grouped_in_order(S):
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=2048, n_heads_kv=4)
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w), route_mode="full_cosine")
+    outs = []
+    for _ in range(2):
+        c = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+        torch.cuda.synchronize()
+        outs.append({k: v.clone() for k, v in c.outputs().items()})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    tg = outs[0]["target"].cpu().numpy()
+    assert ((tg >= 0) & (tg < outs[0]["kept"].shape[2])).all()
