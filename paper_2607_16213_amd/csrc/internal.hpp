@@ -25,6 +25,9 @@ struct ScorePlan {
   int rows_per_group;  // rows held in registers by one pass (16 * row blocks)
   int nrg;           // row groups
   int rpad;          // nrg * rows_per_group
+  int tiled;         // 1: shared-tile passes (bf16, at most 128 window rows)
+  int chunk_keys2;   // shared-tile pass 2: keys per workgroup (outputs staged in LDS)
+  int nchunks2;      // shared-tile pass 2: chunks per KV head
   size_t part_off, stats_off, c_off, bytes;
 };
 
