@@ -155,6 +155,215 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
   }
 }
 
+// bf16 variant with the kept rows shared through LDS.  A workgroup holds 256
+// evicted rows (64 per wave, the MFMA A operand in registers) and streams the
+// head's kept rows in tiles of 64: each thread gathers 1/256 of a tile with
+// 16-byte loads, kMatchDepth tiles ahead, the kept positions one lap further
+// ahead still, and stores it XOR-swizzled into one of two LDS stages that all
+// four waves read as the B operand.  The running argmax compares
+// dot * (1 / ||v_i||) only: the evicted row's own norm does not change its
+// argmax and is applied once, to the winner, for the gate.
+constexpr int kMT = 64;          // kept rows per tile
+constexpr int kMatchDepth = 2;   // tiles of loads in flight per thread
+constexpr int kMatchTiledRB = 4; // 16-row blocks of evicted rows per wave
+
+template <int D>
+struct MGeo {
+  static constexpr int RB = D * 2;
+  static constexpr int NCHUNK = RB / 16;
+  static constexpr int NCH = RB / 64;
+  static constexpr int TILE = kMT * RB;
+  static constexpr int LPT = TILE / (kThreads * 16);
+  static_assert(LPT >= 1 && TILE % (kThreads * 16) == 0, "tile must split evenly over the workgroup");
+};
+
+template <int D>
+__device__ __forceinline__ void mpiece(int j, int tid, int& row, int& ch) {
+  const int off = (j * kThreads + tid) * 16;
+  row = off / MGeo<D>::RB;
+  ch = (off % MGeo<D>::RB) / 16;
+}
+
+template <int D>
+__device__ __forceinline__ int mswz(int row, int ch) {
+  return row * MGeo<D>::RB + ((ch ^ (row & (MGeo<D>::NCHUNK - 1))) * 16);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void cosine_match_tiled(MatchArgs a) {
+  using Geo = MGeo<D>;
+  constexpr int NCH = Geo::NCH, LPT = Geo::LPT, NRB = kMatchTiledRB;
+  __shared__ __align__(16) char lds[2][Geo::TILE];
+  __shared__ float s_inv[2][kMT];    // 1 / ||v_i|| of the tile's kept rows
+  __shared__ float s_off[2][kMT];    // 0, or -inf past the last kept slot
+  const int64_t head = blockIdx.y;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int n = a.n, m = a.m, ne = n - m;
+  const int r0 = (blockIdx.x * kWaves + wave) * NRB * 16;
+  const bool active = r0 < ne;
+  const char* Vh = a.V + (size_t)head * n * Geo::RB;
+  const float* vnh = a.vnorm + (size_t)head * n;
+  const int32_t* kh = a.kept + (size_t)head * m;
+  const int32_t* eh = a.evicted + (size_t)head * ne;
+
+  Chunk16 q[NRB][NCH];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    const int pos = eh[min(r0 + rb * 16 + col, ne - 1)];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) q[rb][c] = load16(Vh + (size_t)pos * Geo::RB + (c * 4 + grp) * 16);
+  }
+  float best[NRB][4];
+  int bidx[NRB][4];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      best[rb][i] = kNegInf;
+      bidx[rb][i] = 0;
+    }
+
+  const int ntiles = (m + kMT - 1) / kMT;
+  // register rings: kept positions (one lap ahead of the data), data, norms
+  int ix[kMatchDepth][LPT], ixn[kMatchDepth];
+  Chunk16 rk[kMatchDepth][LPT];
+  float rn[kMatchDepth];
+  auto load_pos = [&](int slot, int tile) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      int row, ch;
+      mpiece<D>(j, tid, row, ch);
+      ix[slot][j] = kh[min(tile * kMT + row, m - 1)];
+    }
+    ixn[slot] = kh[min(tile * kMT + (tid & (kMT - 1)), m - 1)];
+  };
+  auto load_data = [&](int slot) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      int row, ch;
+      mpiece<D>(j, tid, row, ch);
+      rk[slot][j] = load16(Vh + (size_t)ix[slot][j] * Geo::RB + ch * 16);
+    }
+    rn[slot] = vnh[ixn[slot]];
+  };
+  auto commit = [&](int slot, int stage, int tile) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      int row, ch;
+      mpiece<D>(j, tid, row, ch);
+      store16(lds[stage] + mswz<D>(row, ch), rk[slot][j]);
+    }
+    if (tid < kMT) {
+      s_inv[stage][tid] = rn[slot] > 0.f ? 1.f / rn[slot] : 0.f;
+      s_off[stage][tid] = tile * kMT + tid < m ? 0.f : kNegInf;
+    }
+  };
+  // value = fma(dot, 1 / ||v_i||, off): off = -inf masks slots past the end,
+  // so every tile runs the same branch-free code
+  // the MFMAs of column block kk + 1 are issued before the epilogue of block
+  // kk, so the matrix core and the VALU work on independent data
+  auto mfma_block = [&](int stage, int kk, f32x4 (&acc)[NRB]) {
+    const int row = kk * 16 + col;
+    Chunk16 bf[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) bf[c] = *reinterpret_cast<const Chunk16*>(lds[stage] + mswz<D>(row, c * 4 + grp));
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+      acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) acc[rb] = Mma<bf16_t>::step(q[rb][c], bf[c], acc[rb]);
+    }
+  };
+  auto epilogue = [&](int stage, int tile, int kk, const f32x4 (&acc)[NRB]) {
+    const int row = kk * 16 + col;
+    const int slot = tile * kMT + row;
+    const float icur = s_inv[stage][row], off = s_off[stage][row];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // slots rise along the stream: a strict compare keeps the lower slot on ties
+        const float v = fmaf(acc[rb][i], icur, off);
+        const bool gt = v > best[rb][i];
+        best[rb][i] = gt ? v : best[rb][i];
+        bidx[rb][i] = gt ? slot : bidx[rb][i];
+      }
+  };
+  auto body = [&](int stage, int tile) {
+    f32x4 acc[2][NRB];
+    mfma_block(stage, 0, acc[0]);
+#pragma unroll
+    for (int kk = 0; kk < kMT / 16; ++kk) {
+      if (kk + 1 < kMT / 16) mfma_block(stage, kk + 1, acc[(kk + 1) & 1]);
+      epilogue(stage, tile, kk, acc[kk & 1]);
+    }
+  };
+
+  // prologue: positions for tiles 0 .. 2*depth-1, data for tiles 0 .. depth-1
+#pragma unroll
+  for (int p = 0; p < kMatchDepth; ++p) load_pos(p, p);
+#pragma unroll
+  for (int p = 0; p < kMatchDepth; ++p) load_data(p);
+#pragma unroll
+  for (int p = 0; p < kMatchDepth; ++p) load_pos(p, p + kMatchDepth);
+  commit(0, 0, 0);
+  load_data(0);
+  load_pos(0, 2 * kMatchDepth);
+  __syncthreads();
+  // every load, LDS store and tile body runs on every trip: past the end the
+  // loads re-read the last kept row and the masks turn those slots to -inf,
+  // so the loop has no branches and the compiler waits only for the oldest slot
+  for (int i = 0; i < ntiles; i += kMatchDepth) {
+#pragma unroll
+    for (int u = 0; u < kMatchDepth; ++u) {
+      const int tile = i + u;
+      const int nu = (u + 1) % kMatchDepth;    // a constant once the loop is unrolled
+      commit(nu, (tile + 1) & 1, tile + 1);
+      load_data(nu);
+      load_pos(nu, tile + 1 + 2 * kMatchDepth);
+      body(tile & 1, tile);
+      __syncthreads();
+    }
+  }
+
+  if (!active) return;
+  // merge the 16 lanes (slot subsets) of each row: larger value, then lower slot
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        const float ob = xor_shfl(best[rb][i], off);
+        const int oi = xor_shfl(bidx[rb][i], off);
+        if (ob > best[rb][i] || (ob == best[rb][i] && oi < bidx[rb][i])) {
+          best[rb][i] = ob;
+          bidx[rb][i] = oi;
+        }
+      }
+  if (col == 0) {
+    int32_t* th = a.target + (size_t)head * ne;
+    float* gh = a.gate + (size_t)head * ne;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = r0 + rb * 16 + grp * 4 + i;
+        if (e < ne) {
+          const float vn = vnh[eh[e]];
+          const float cosv = vn > 0.f ? best[rb][i] * (1.f / vn) : 0.f;
+          float g;
+          if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
+          else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
+          else g = fminf(1.f, fmaxf(0.f, (cosv - a.tau) * a.inv_temp));
+          th[e] = bidx[rb][i];
+          gh[e] = g;
+        }
+      }
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(int32_t* p, int64_t count) {
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i < count) p[i] = 0;
@@ -386,11 +595,11 @@ hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float t
   a.gate_mode = gate_mode;
   a.tau = tau;
   a.inv_temp = 1.f / temp;
-  const int rows_per_block = kWaves * kMatchRowBlocks * 16;
+  const int rows_per_block = kWaves * (dtype == SELKV_BF16 ? kMatchTiledRB : kMatchRowBlocks) * 16;
   const dim3 grid((ne + rows_per_block - 1) / rows_per_block, (unsigned)s.heads);
   if (dtype == SELKV_BF16) {
-    if (s.d == 128) hipLaunchKernelGGL((cosine_match_kernel<bf16_t, 128>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((cosine_match_kernel<bf16_t, 64>), grid, dim3(kThreads), 0, st, a);
+    if (s.d == 128) hipLaunchKernelGGL((cosine_match_tiled<128>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((cosine_match_tiled<64>), grid, dim3(kThreads), 0, st, a);
   } else {
     if (s.d == 128) hipLaunchKernelGGL((cosine_match_kernel<float, 128>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((cosine_match_kernel<float, 64>), grid, dim3(kThreads), 0, st, a);
