@@ -28,7 +28,15 @@ Readings taken where the paper is silent or garbled:
     pre-merge target value;
   * keys are not merged, only gathered (Eq. 5 defines only values);
   * bias (Eq. 6): natural log, alpha * ln R_i added after the softmax scale,
-    per KV head (the per-head rule of Sec. 3.6).
+    per KV head (the per-head rule of Sec. 3.6);
+  * GQA union mode (Sec. 3.3 union-selection paragraph, Sec. 3.6 GQA rule):
+    each KV head's top-m_s set by its own scores, the union over the KV
+    heads of one cache, trimmed to m_s by the mean score across KV heads
+    (ties to the lower position); since every head contributes m_s tokens
+    the union never falls short, so the shared kept set has exactly m
+    entries.  The mean is taken in float32 in head order because it decides
+    integers (which tokens survive) and the GPU decides in float32.  R is
+    averaged across KV heads and alpha * ln(mean R) is shared by them.
 """
 from __future__ import annotations
 
@@ -148,6 +156,48 @@ def select(s: np.ndarray, n: int, m: int, mr: int):
     is_kept[kept] = True
     evicted = np.flatnonzero(~is_kept).astype(np.int64)
     return kept, evicted
+
+
+def union_mean_score(s_heads: np.ndarray) -> np.ndarray:
+    """Mean aggregate score across the KV heads of one cache (the trimming
+    key of Sec. 3.3's union selection), in float32: the heads' scores are
+    added in head order and the sum divided by the head count."""
+    s_heads = np.asarray(s_heads, dtype=np.float32)
+    acc = np.zeros(s_heads.shape[1], dtype=np.float32)
+    for h in range(s_heads.shape[0]):
+        acc = (acc + s_heads[h]).astype(np.float32)
+    return (acc / np.float32(s_heads.shape[0])).astype(np.float32)
+
+
+def select_union(s_heads: np.ndarray, n: int, m: int, mr: int):
+    """Union selection for GQA models (Sec. 3.3): every KV head picks its own
+    top-m_s candidates (Eq. 2 on its scores); a candidate is kept when any
+    KV head picks it; if that union holds more than m_s candidates, only the
+    m_s with the largest mean score across KV heads stay (equal means: the
+    lower position).  The last m_r positions are kept as in Eq. 2.  One kept
+    set is shared by all KV heads.
+
+    s_heads [H_kv, n - m_r] are the per-KV-head scores.  Returns (kept [m],
+    evicted [n - m]) ascending int64 positions.
+    """
+    s_heads = np.asarray(s_heads)
+    H, n_cand = s_heads.shape
+    assert n_cand == n - mr
+    ms = m - mr
+    union = np.zeros(n_cand, dtype=bool)
+    for h in range(H):
+        kept_h, _ = select(np.asarray(s_heads[h], dtype=np.float64), n, m, mr)
+        union[kept_h[kept_h < n_cand]] = True
+    cand = np.flatnonzero(union)
+    assert cand.shape[0] >= ms, "each head contributes m_s candidates"
+    if cand.shape[0] > ms:
+        mean = union_mean_score(s_heads).astype(np.float64)
+        order = np.lexsort((cand, -mean[cand]))      # larger mean first, then lower position
+        cand = np.sort(cand[order[:ms]])
+    kept = np.concatenate([cand, np.arange(n_cand, n)]).astype(np.int64)
+    is_kept = np.zeros(n, dtype=bool)
+    is_kept[kept] = True
+    return kept, np.flatnonzero(~is_kept).astype(np.int64)
 
 
 # --------------------------------------------------------------------------
@@ -276,6 +326,29 @@ def ratio_bias(a: np.ndarray, kept: np.ndarray, evicted: np.ndarray, target: np.
     a_kept = a[kept]
     R = (a_kept + absorbed) / a_kept
     return alpha * np.log(R)
+
+
+def ratio_bias_union(a_heads: np.ndarray, kept: np.ndarray, evicted: np.ndarray, targets: np.ndarray,
+                     gates: np.ndarray, alpha: float) -> np.ndarray:
+    """Sec. 3.6, GQA rule: with one kept set shared by the KV heads, each
+    head's ratio R_{h,i} of Eq. 6 is averaged across the KV heads and
+    alpha * ln(mean_h R_{h,i}) is the bias of every head.
+
+    a_heads [H, n]; targets, gates [H, n - m] (each head routes its own
+    evicted tokens).  Returns bias [m], shared by the heads.
+    """
+    H = a_heads.shape[0]
+    R = np.zeros((H, kept.shape[0]), dtype=np.float64)
+    for h in range(H):
+        a = np.asarray(a_heads[h], dtype=np.float64)
+        absorbed = np.zeros(kept.shape[0], dtype=np.float64)
+        for e, j in enumerate(evicted):
+            t = int(targets[h][e])
+            if t >= 0:
+                absorbed[t] += gates[h][e] * a[j]
+        a_kept = a[kept]
+        R[h] = (a_kept + absorbed) / a_kept
+    return alpha * np.log(R.mean(axis=0))
 
 
 # --------------------------------------------------------------------------

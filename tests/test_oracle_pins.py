@@ -388,3 +388,84 @@ def test_attention_sag_restored_exactly_with_alpha_one(seed):
     # without any compensation the cache is the plain eviction result
     nob = O.decode(q, out["k_out"][None], out["v_out"][None], None, G, sc)
     assert np.abs(nob - full).max() > 1e-6
+
+
+# ------------------------------------------------------------------ GQA union mode (Sec. 3.3, Sec. 3.6)
+def test_union_selection_hand_worked():
+    """Sec. 3.3 union selection on a hand-worked case: the trim keeps the top
+    mean scores among tokens some head picked, never a token no head picked."""
+    c = GOLD["union_selection"]
+    n, mr = c["n"], c["recent"]
+    m, mr2, ms = O.budget(n, c["budget_ratio"], mr)
+    kept, ev = O.select_union(np.array(c["scores"], dtype=np.float32), n, m, mr2)
+    assert kept.tolist() == c["kept"] and ev.tolist() == c["evicted"]
+
+
+def test_union_selection_reduces_to_per_head_cases():
+    rng = np.random.default_rng(11)
+    n, m, mr = 64, 24, 4
+    s = rng.random((1, n - mr)).astype(np.float32)
+    # a single KV head: the union is that head's own selection
+    assert [x.tolist() for x in O.select_union(s, n, m, mr)] == [x.tolist() for x in O.select(s[0].astype(np.float64), n, m, mr)]
+    # identical heads: every head picks the same set
+    s3 = np.repeat(s, 3, axis=0)
+    assert [x.tolist() for x in O.select_union(s3, n, m, mr)] == [x.tolist() for x in O.select(s[0].astype(np.float64), n, m, mr)]
+    # heads picking disjoint sets that together are exactly m_s long stay whole
+    s2 = np.zeros((2, n - mr), dtype=np.float32)
+    ms = m - mr
+    s2[0, : ms // 2] = 1.0
+    s2[1, ms // 2: ms] = 1.0
+    kept, _ = O.select_union(s2, n, m, mr)
+    assert kept[:ms].tolist() == list(range(ms))
+
+
+def test_union_selection_properties_random():
+    """Shared set of exactly m; every kept candidate was picked by some head;
+    no dropped union member has a larger mean (or an equal mean at a lower
+    position) than a kept one."""
+    rng = np.random.default_rng(5)
+    for trial in range(20):
+        H = int(rng.integers(2, 6))
+        n = int(rng.integers(20, 120))
+        mr = int(rng.integers(0, 6))
+        rho = float(rng.uniform(0.1, 0.9))
+        m, mr2, ms = O.budget(n, rho, mr)
+        s = rng.integers(0, 6, size=(H, n - mr2)).astype(np.float32) / 4.0   # many exact ties
+        kept, ev = O.select_union(s, n, m, mr2)
+        assert kept.shape[0] == m and np.array_equal(np.sort(np.concatenate([kept, ev])), np.arange(n))
+        picked = np.zeros(n - mr2, dtype=bool)
+        for h in range(H):
+            kh, _ = O.select(s[h].astype(np.float64), n, m, mr2)
+            picked[kh[kh < n - mr2]] = True
+        cand = kept[kept < n - mr2]
+        assert picked[cand].all()
+        mean = s.astype(np.float64).mean(axis=0)
+        dropped = np.flatnonzero(picked & ~np.isin(np.arange(n - mr2), cand))
+        for j in dropped:
+            for i in cand:
+                assert (mean[i], -i) > (mean[j], -j)
+
+
+def test_union_ratio_bias_hand_worked():
+    """Sec. 3.6 GQA rule: the bias is alpha * ln of the mean of the heads'
+    ratios, not the mean of their per-head biases."""
+    c = GOLD["union_ratio_bias"]
+    got = O.ratio_bias_union(np.array(c["a"]), np.array(c["kept"]), np.array(c["evicted"]),
+                             np.array(c["targets"]), np.array(c["gates"]), c["alpha"])
+    want = [c["alpha"] * math.log(r) for r in c["mean_R"]]
+    assert np.allclose(got, want, rtol=0, atol=1e-15)
+    per_head = [O.ratio_bias(np.array(c["a"][h]), np.array(c["kept"]), np.array(c["evicted"]),
+                             np.array(c["targets"][h]), np.array(c["gates"][h]), c["alpha"]) for h in range(2)]
+    assert not np.allclose(got, np.mean(per_head, axis=0))
+
+
+def test_union_ratio_bias_single_head_is_per_head():
+    rng = np.random.default_rng(3)
+    n = 40
+    a = rng.random(n) + 0.1
+    kept = np.sort(rng.choice(n, 10, replace=False))
+    ev = np.setdiff1d(np.arange(n), kept)
+    tg = rng.integers(-1, 10, size=ev.shape[0])
+    g = rng.random(ev.shape[0])
+    one = O.ratio_bias_union(a[None], kept, ev, tg[None], g[None], 0.5)
+    assert np.allclose(one, O.ratio_bias(a, kept, ev, tg, g, 0.5), rtol=1e-14, atol=1e-15)
