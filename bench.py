@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--print-source-hash", action="store_true", help="print the decode source hash and exit")
     ap.add_argument("--full-cosine-layers", type=int, default=1,
                     help="layers timed with the all-pairs cosine routing variant (0 = skip)")
+    ap.add_argument("--no-union", action="store_true", help="skip the GQA union-mode compression timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
     return ap.parse_args()
@@ -253,6 +254,47 @@ def measure(job, steps, warmup):
     return wall, st
 
 
+def measure_union(job, reps=3):
+    """The GQA union mode of Sec. 3.3 / 3.6 (the paper's default for GQA
+    models) on the same resident cache: the four compression calls with one
+    kept set shared by the KV heads of each layer and the ratio averaged
+    across them.  Reuses the job's output buffers (run after the decode
+    measurements)."""
+    torch, selkv, w = job.torch, job.selkv, job.w
+    p = selkv.params(batch=job.LB, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim, seq_len=w.seq_len,
+                     window=w.window, kv_dtype=w.dtype, budget_ratio=w.budgets[0], select_mode="union")
+    c, dev = job.comp, job.K.device
+    ws_sel = selkv.workspace(p, selkv.CALL_SELECT, dev)
+    ws_bias = selkv.workspace(p, selkv.CALL_BIAS, dev)
+
+    def run(ev=None):
+        if ev: ev[0].record()
+        selkv.score(p, job.Kf, job.Vf, job.Qf, c.score, c.attn, c.vnorm, c.ws_score)
+        if ev: ev[1].record()
+        selkv.select(p, c.score, c.kept, c.evicted, ws_sel)
+        if ev: ev[2].record()
+        selkv.merge(p, job.Kf, job.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
+                    c.ws_merge)
+        if ev: ev[3].record()
+        selkv.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, ws_bias)
+        if ev: ev[4].record()
+
+    run()
+    torch.cuda.synchronize()
+    names = ("score", "select", "merge", "bias")
+    tot = {k: 0.0 for k in names}
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        run(ev)
+        torch.cuda.synchronize()
+        for i, k in enumerate(names):
+            tot[k] += ev[i].elapsed_time(ev[i + 1]) / reps
+    comp_ms = sum(tot.values())
+    return {"compress_ms": round(comp_ms, 4), "compress_tokens_per_s": round(w.seq_len * w.batch / (comp_ms / 1e3), 1),
+            "stages_ms": {k: round(v, 4) for k, v in tot.items()},
+            "note": "select_mode union: per-KV-head top-m_s, union per layer, trim by mean score; R averaged over KV heads"}
+
+
 def measure_full_cosine(job, layers, reps=3):
     """The all-pairs cosine routing variant of the merge call on the first
     `layers` layers of the resident workload, fed the compressed job's own
@@ -355,6 +397,8 @@ def main():
 
     if args.full_cosine_layers > 0:
         out["full_cosine_routing"] = measure_full_cosine(job, min(args.full_cosine_layers, w.layers))
+    if not args.no_union:
+        out["gqa_union"] = measure_union(job)
 
     traffic = read_traffic()
     out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define SELKV_ABI_VERSION 1
+#define SELKV_ABI_VERSION 2
 
 typedef enum selkv_status {
   SELKV_OK = 0,
@@ -77,6 +77,17 @@ typedef enum selkv_route_mode {
   SELKV_ROUTE_BUCKET = 0,
   SELKV_ROUTE_FULL_COSINE = 1
 } selkv_route_mode;
+
+/* Token selection of Sec. 3.3.  PER_HEAD: every KV head keeps its own
+ * top-m_s set (Eq. 2; the MHA rule, and per-KV-head selection for GQA).
+ * UNION: the GQA rule - each KV head picks its top-m_s, the union over the
+ * n_heads_kv heads of one cache is trimmed to m_s by the mean score across
+ * those heads, and that one kept set is shared by all of them; selkv_bias
+ * then averages R across the heads (Sec. 3.6). */
+typedef enum selkv_select_mode {
+  SELKV_SELECT_PER_HEAD = 0,
+  SELKV_SELECT_UNION = 1
+} selkv_select_mode;
 
 /* Which call a workspace size is asked for. */
 typedef enum selkv_call {
@@ -108,6 +119,7 @@ typedef struct selkv_params {
   float gate_threshold;      /* tau: g = clamp((sim - tau) / T, 0, 1); tau = 0, T = 1 is max(sim, 0) */
   float gate_temperature;    /* T > 0 */
   double budget_ratio;       /* rho in (0, 1]; m = floor(rho * n) computed in IEEE double (Sec. 3.1) */
+  int32_t select_mode;       /* selkv_select_mode (default PER_HEAD) */
 } selkv_params;
 
 /* Fill `p` with the paper's defaults (App. F: W = 32, K = 5, B = 32,
@@ -149,14 +161,22 @@ SELKV_API selkv_status selkv_score(const selkv_params* p, const void* K, const v
                                    float* score, float* attn, float* vnorm, void* ws, size_t ws_bytes,
                                    hipStream_t stream);
 
-/* Step 2 of Algorithm 1: per-head selection (Sec. 3.3, Eq. 2).
+/* Step 2 of Algorithm 1: token selection (Sec. 3.3, Eq. 2).
  *
- * Per KV head, keeps the m_s candidates with the largest score (equal
- * scores: the lower position wins) plus the m_r' most recent positions.
+ * PER_HEAD: per KV head, keeps the m_s candidates with the largest score
+ * (equal scores: the lower position wins) plus the m_r' most recent
+ * positions.  UNION (GQA): per cache b, each of the H_kv heads picks its
+ * top-m_s as above; a candidate picked by any head is in the union; the
+ * union is cut to its m_s candidates of largest mean score across the heads
+ * (the mean is the fp32 sum in head order divided by H_kv; equal means: the
+ * lower position wins); that set plus the recent positions is written for
+ * every head of the cache.  Every head contributes m_s candidates, so the
+ * union is never short and each head keeps exactly m entries.
  * In:  score [B, H_kv, n - m_r'] fp32 (NaN is outside the contract)
  * Out: kept_idx [B, H_kv, m] and evicted_idx [B, H_kv, n - m], int32
  *      positions, each ascending; together a partition of 0..n-1.
- * Workspace: selkv_workspace_size(p, SELKV_CALL_SELECT, 0). */
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_SELECT, 0) (0 for
+ *      PER_HEAD; the union flags, means and shared set for UNION). */
 SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, int32_t* kept_idx,
                                     int32_t* evicted_idx, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -191,13 +211,17 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
  * R_s = (a_i + sum_{j->s} g_j a_j) / a_i for kept slot s (position i), and
  * bias[s] = alpha * ln R_s, the per-KV-head logit bias that decode adds
  * (the per-head rule of Sec. 3.6).  R_s = 1 (bias exactly 0) where nothing
- * was absorbed.
+ * was absorbed.  With select_mode UNION (one kept set shared by the H_kv
+ * heads of a cache, the GQA rule) R is averaged across those heads first:
+ * bias[b, h, s] = alpha * ln(mean_h' R_{h', s}) for every h, the mean being
+ * the fp32 sum of (R - 1) in head order divided by H_kv.
  * In:  attn [B, H_kv, n]; kept_idx, evicted_idx; target, gate (from
  *      selkv_merge with the same params: under BUCKET routing every routed
  *      token lies in its target's bucket, which this call relies on; under
  *      FULL_COSINE any target slot is allowed).
  * Out: bias [B, H_kv, m] fp32.
- * Workspace: selkv_workspace_size(p, SELKV_CALL_BIAS, 0). */
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_BIAS, 0) (UNION adds the
+ *      per-head ratios). */
 SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,
                                   const int32_t* evicted_idx, const int32_t* target, const float* gate,
                                   float* bias, void* ws, size_t ws_bytes, hipStream_t stream);
@@ -208,16 +232,15 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
  * out[b, h] = sum_s softmax_s(scale * q[b, h] . K[b, h/G, s] + bias[b, h/G, s]) V[b, h/G, s]
  * over the cache_len entries of KV head h/G.  bias may be NULL (plain
  * attention, e.g. the uncompressed cache); a zero bias gives bitwise the
- * same result as NULL.  Split-K over the cache with an in-order combine in
- * the same launch.
+ * same result as NULL.  Split-K over the cache; a second kernel on the same
+ * stream combines the splits in split order.
  * In:  q [B, H_kv*G, d] (kv_dtype); K, V [B, H_kv, cache_len, d] (kv_dtype);
  *      bias [B, H_kv, cache_len] fp32 or NULL.  Uses params batch,
  *      n_heads_kv, group (1..8), head_dim, kv_dtype and scale only.
  * Out: out [B, H_kv*G, d] fp32.
- * Workspace: selkv_workspace_size(p, SELKV_CALL_DECODE, cache_len) bytes.
- *      It holds per-head completion counters and MUST be zero-filled before
- *      its first use; every call leaves the counters at zero again.  Calls
- *      that may overlap in time need separate workspaces. */
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_DECODE, cache_len) bytes
+ *      for the per-split partials; no initialisation is needed.  Calls that
+ *      may overlap in time need separate workspaces. */
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream);

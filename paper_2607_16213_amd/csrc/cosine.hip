@@ -461,6 +461,7 @@ struct GroupMergeArgs {
   float* bias;
   int n, m;
   float alpha;
+  int raw;   // bias mode: write wsum / a_s (R - 1) instead of alpha * ln R
 };
 
 // One wave per kept slot: Eq. 5 (and the Eq. 6 bias when `bias` is set) over
@@ -535,7 +536,8 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     }
   }
   if (!VALUES) {
-    if (lane == 0) a.bias[(size_t)head * m + s] = wsum > 0.f ? a.alpha * log1pf(wsum / a_s) : 0.f;
+    if (lane == 0)
+      a.bias[(size_t)head * m + s] = wsum > 0.f ? (a.raw ? wsum / a_s : a.alpha * log1pf(wsum / a_s)) : 0.f;
     return;
   }
 #pragma unroll
@@ -626,7 +628,8 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
 
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
-                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, hipStream_t st) {
+                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
+                              hipStream_t st) {
   const char* w = static_cast<const char*>(ws);
   GroupMergeArgs a{};
   a.K = static_cast<const char*>(K);
@@ -643,6 +646,7 @@ hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, con
   a.n = s.n;
   a.m = s.m;
   a.alpha = alpha;
+  a.raw = raw ? 1 : 0;
   const dim3 grid((s.m + kWaves - 1) / kWaves, (unsigned)s.heads);
   const bool values = bias == nullptr;
 #define SELKV_GM(T, D)                                                                        \

@@ -12,6 +12,7 @@ namespace selkv {
 // Validated, derived sizes of one problem.
 struct Shape {
   int64_t heads;     // batch * n_heads_kv
+  int hkv;           // n_heads_kv (heads of one cache)
   int n, d, G, W, R; // R = G * W window rows per KV head
   int m, mr, ms;     // budget of Sec. 3.1
   int n_cand;        // n - mr
@@ -44,7 +45,15 @@ struct GroupPlan {
   size_t off_off, cursor_off, list_off, bytes;
 };
 
+// Workspace of the GQA union mode: flags, mean keys and the shared set per
+// cache for selection; the per-head R - 1 for the bias.
+struct UnionPlan {
+  size_t flag_off, key_off, kept_off, ev_off, select_bytes;
+  size_t ratio_bytes;
+};
+
 ScorePlan plan_score(const Shape& s, int dtype);
+UnionPlan plan_union(const Shape& s);
 GroupPlan plan_group(const Shape& s);
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G);
 size_t bucket_offsets_bytes(const Shape& s);
@@ -59,16 +68,21 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
                                const void* K, const void* V, const float* attn, const float* vnorm,
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
                                void* V_out, int32_t* target, float* gate, hipStream_t st);
+// raw: write R - 1 = absorbed / a instead of alpha * ln R (the union mode averages it)
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
-                              const float* gate, float* bias, hipStream_t st);
+                              const float* gate, float* bias, bool raw, hipStream_t st);
 hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
                                const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
                                float* gate, hipStream_t st);
 hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st);
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
-                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, hipStream_t st);
+                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
+                              hipStream_t st);
+hipError_t launch_union_select(const Shape& s, const UnionPlan& p, const float* score, int32_t* kept,
+                               int32_t* evicted, void* ws, hipStream_t st);
+hipError_t launch_union_bias(const Shape& s, const float* r1, float* bias, float alpha, hipStream_t st);
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int d, int G, int dtype, float scale,
                          const DecodePlan& plan, const void* q, const void* K, const void* V, const float* bias,
                          float* out, void* ws, hipStream_t st);

@@ -244,6 +244,7 @@ struct BiasArgs {
   float* bias;
   int n, m, nb, B;
   float alpha;
+  int raw;   // write absorbed / a (R - 1) instead of alpha * ln R
 };
 
 // One wave per kBiasBuckets consecutive buckets.  For each bucket lane e
@@ -322,7 +323,9 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
         if (t == k) absorbed += c;
       }
     }
-    if (k < k1[bi]) a.bias[(size_t)head * m + k] = absorbed > 0.f ? a.alpha * log1pf(absorbed / a_k[bi]) : 0.f;
+    if (k < k1[bi])
+      a.bias[(size_t)head * m + k] =
+          absorbed > 0.f ? (a.raw ? absorbed / a_k[bi] : a.alpha * log1pf(absorbed / a_k[bi])) : 0.f;
   }
 }
 
@@ -378,8 +381,9 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
 
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
-                              const float* gate, float* bias, hipStream_t st) {
+                              const float* gate, float* bias, bool raw, hipStream_t st) {
   BiasArgs a{};
+  a.raw = raw ? 1 : 0;
   a.attn = attn;
   a.kept = kept;
   a.evicted = evicted;

@@ -30,6 +30,7 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
     return SELKV_EINVAL;
   if (p->gate_mode < SELKV_GATE_COSINE || p->gate_mode > SELKV_GATE_MERGE_ALL) return SELKV_EINVAL;
   if (p->route_mode != SELKV_ROUTE_BUCKET && p->route_mode != SELKV_ROUTE_FULL_COSINE) return SELKV_EINVAL;
+  if (p->select_mode != SELKV_SELECT_PER_HEAD && p->select_mode != SELKV_SELECT_UNION) return SELKV_EINVAL;
   const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
   if (heads > 65535) return SELKV_EUNSUPPORTED;              // grid y dimension
   const int64_t R = (int64_t)p->group * p->window;
@@ -38,6 +39,7 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
   const int m = (int)md;
   if (m < 1) return SELKV_EINVAL;
   s->heads = heads;
+  s->hkv = p->n_heads_kv;
   s->n = p->seq_len;
   s->d = p->head_dim;
   s->G = p->group;
@@ -56,6 +58,15 @@ float eff_scale(const selkv_params* p) { return p->scale > 0.f ? p->scale : 1.f 
 size_t elem_size(const selkv_params* p) { return p->kv_dtype == SELKV_BF16 ? 2 : 4; }
 
 selkv_status hip_status(hipError_t e) { return e == hipSuccess ? SELKV_OK : SELKV_EHIP; }
+
+bool is_union(const selkv_params* p) { return p->select_mode == SELKV_SELECT_UNION; }
+
+// bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
+size_t bias_base_bytes(const selkv_params* p, const Shape& s) {
+  return p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
+}
+
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 selkv_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return SELKV_OK;
@@ -89,6 +100,7 @@ SELKV_API void selkv_params_init(selkv_params* p) {
   p->gate_threshold = 0.f;
   p->gate_temperature = 1.f;
   p->budget_ratio = 0.25;
+  p->select_mode = SELKV_SELECT_PER_HEAD;
 }
 
 SELKV_API selkv_status selkv_budget(const selkv_params* p, int32_t* m, int32_t* m_recent, int32_t* m_select) {
@@ -115,10 +127,13 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
   if (st != SELKV_OK) return st;
   switch (call) {
     case SELKV_CALL_SCORE: *bytes = plan_score(s, p->kv_dtype).bytes; return SELKV_OK;
-    case SELKV_CALL_SELECT: *bytes = 0; return SELKV_OK;
+    case SELKV_CALL_SELECT: *bytes = is_union(p) ? plan_union(s).select_bytes : 0; return SELKV_OK;
     case SELKV_CALL_MERGE:
-    case SELKV_CALL_BIAS:
       *bytes = p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
+      return SELKV_OK;
+    case SELKV_CALL_BIAS:
+      *bytes = bias_base_bytes(p, s);
+      if (is_union(p)) *bytes = round256(*bytes) + plan_union(s).ratio_bytes;
       return SELKV_OK;
     default: return SELKV_EINVAL;
   }
@@ -142,13 +157,16 @@ SELKV_API selkv_status selkv_score(const selkv_params* p, const void* K, const v
 
 SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, int32_t* kept_idx,
                                     int32_t* evicted_idx, void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   Shape s;
   selkv_status st = make_shape(p, &s);
   if (st != SELKV_OK) return st;
   if (!score || !kept_idx || (!evicted_idx && s.n > s.m)) return SELKV_EINVAL;
   if (!aligned(score, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4)) return SELKV_EALIGN;
+  if (is_union(p)) {
+    const UnionPlan up = plan_union(s);
+    if ((st = check_ws(ws, ws_bytes, up.select_bytes)) != SELKV_OK) return st;
+    return hip_status(launch_union_select(s, up, score, kept_idx, evicted_idx, ws, stream));
+  }
   return hip_status(launch_select(s, score, kept_idx, evicted_idx, stream));
 }
 
@@ -175,7 +193,7 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
     e = launch_group(s, gp, target, ws, stream);
     if (e != hipSuccess) return SELKV_EHIP;
     return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out,
-                                         V_out, nullptr, 0.f, stream));
+                                         V_out, nullptr, 0.f, false, stream));
   }
   const size_t need = bucket_offsets_bytes(s);
   if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
@@ -199,21 +217,28 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
   if (!aligned(attn, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
       !aligned(gate, 4) || !aligned(bias, 4))
     return SELKV_EALIGN;
+  // union mode: the routing kernels write each head's R - 1 into the
+  // workspace and one more pass averages it over the heads of each cache
+  const bool uni = is_union(p);
+  const size_t base = bias_base_bytes(p, s);
+  const size_t need = uni ? round256(base) + plan_union(s).ratio_bytes : base;
+  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
+  float* dst = uni ? reinterpret_cast<float*>(static_cast<char*>(ws) + round256(base)) : bias;
+  hipError_t e;
   if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {
     const GroupPlan gp = plan_group(s);
-    if ((st = check_ws(ws, ws_bytes, gp.bytes)) != SELKV_OK) return st;
-    hipError_t e = launch_group(s, gp, target, ws, stream);
+    e = launch_group(s, gp, target, ws, stream);
     if (e != hipSuccess) return SELKV_EHIP;
-    return hip_status(launch_group_merge(s, gp, p->kv_dtype, nullptr, nullptr, attn, kept_idx, evicted_idx, gate, ws,
-                                         nullptr, nullptr, bias, p->alpha, stream));
+    e = launch_group_merge(s, gp, p->kv_dtype, nullptr, nullptr, attn, kept_idx, evicted_idx, gate, ws, nullptr,
+                           nullptr, dst, p->alpha, uni, stream);
+  } else {
+    int32_t* offs = static_cast<int32_t*>(ws);
+    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    e = launch_bias_bucket(s, p->bucket, p->alpha, attn, kept_idx, evicted_idx, offs, target, gate, dst, uni, stream);
   }
-  const size_t need = bucket_offsets_bytes(s);
-  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
-  int32_t* offs = static_cast<int32_t*>(ws);
-  hipError_t e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
-  if (e != hipSuccess) return SELKV_EHIP;
-  e = launch_bias_bucket(s, p->bucket, p->alpha, attn, kept_idx, evicted_idx, offs, target, gate, bias, stream);
-  return hip_status(e);
+  if (e != hipSuccess || !uni) return hip_status(e);
+  return hip_status(launch_union_bias(s, dst, bias, p->alpha, stream));
 }
 
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,

@@ -19,11 +19,14 @@ LIB_PATH = os.path.join(_PKG, "libselkv.so")
 F32, BF16 = 0, 1
 GATE_COSINE, GATE_DROP, GATE_MERGE_ALL = 0, 1, 2
 ROUTE_BUCKET, ROUTE_FULL_COSINE = 0, 1
+SELECT_PER_HEAD, SELECT_UNION = 0, 1
+ABI_VERSION = 2
 CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE = range(5)
 STATUS = {0: "SELKV_OK", 1: "SELKV_EINVAL", 2: "SELKV_EDTYPE", 3: "SELKV_EUNSUPPORTED", 4: "SELKV_EALIGN",
           5: "SELKV_EWORKSPACE", 6: "SELKV_EHIP"}
 GATE_MODES = {"cosine": GATE_COSINE, "drop": GATE_DROP, "merge_all": GATE_MERGE_ALL}
 ROUTE_MODES = {"bucket": ROUTE_BUCKET, "full_cosine": ROUTE_FULL_COSINE}
+SELECT_MODES = {"per_head": SELECT_PER_HEAD, "union": SELECT_UNION}
 
 
 class SelkvError(RuntimeError):
@@ -52,6 +55,7 @@ class Params(ctypes.Structure):
         ("gate_threshold", ctypes.c_float),
         ("gate_temperature", ctypes.c_float),
         ("budget_ratio", ctypes.c_double),
+        ("select_mode", ctypes.c_int32),
     ]
 
 
@@ -81,6 +85,8 @@ def _load():
 
 
 lib = _load()
+if lib.selkv_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} has ABI version {lib.selkv_abi_version()}, this binding expects {ABI_VERSION}")
 
 
 def params(**kw) -> Params:
@@ -92,6 +98,8 @@ def params(**kw) -> Params:
             v = GATE_MODES[v]
         if k == "route_mode" and isinstance(v, str):
             v = ROUTE_MODES[v]
+        if k == "select_mode" and isinstance(v, str):
+            v = SELECT_MODES[v]
         if k == "kv_dtype" and isinstance(v, (str, torch.dtype)):
             v = BF16 if v in ("bf16", torch.bfloat16) else F32
         if not hasattr(p, k):
@@ -232,13 +240,14 @@ class Compressor:
         self.gate = torch.empty((B, H, n - m), dtype=f32, device=device)
         self.bias = torch.empty((B, H, m), dtype=f32, device=device)
         self.ws_score = workspace(p, CALL_SCORE, device)
+        self.ws_select = workspace(p, CALL_SELECT, device)
         self.ws_merge = workspace(p, CALL_MERGE, device)
         self.ws_bias = workspace(p, CALL_BIAS, device)
 
     def run(self, K, V, Qwin, stream=None):
         p = self.p
         score(p, K, V, Qwin, self.score, self.attn, self.vnorm, self.ws_score, stream)
-        select(p, self.score, self.kept, self.evicted, None, stream)
+        select(p, self.score, self.kept, self.evicted, self.ws_select, stream)
         merge(p, K, V, self.attn, self.vnorm, self.kept, self.evicted, self.K_out, self.V_out, self.target,
               self.gate, self.ws_merge, stream)
         bias(p, self.attn, self.kept, self.evicted, self.target, self.gate, self.bias, self.ws_bias, stream)

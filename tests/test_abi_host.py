@@ -63,7 +63,7 @@ def test_params_init_defaults(S):
     assert p.struct_size == ctypes.sizeof(S.Params)
     assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
     assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
-    assert S.lib.selkv_abi_version() == 1
+    assert S.lib.selkv_abi_version() == 2
     assert S.lib.selkv_status_string(0) == b"success"
 
 
@@ -124,3 +124,15 @@ def test_call_validation_before_launch(S):
     assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, 16, None) == 5
     assert m(ctypes.byref(pf), fake, fake, fake, fake, fake, fake, mis, fake, fake, fake, fake, 1 << 30, None) == 4
     assert S.workspace_bytes(pf, S.CALL_MERGE) > S.workspace_bytes(S.params(seq_len=256), S.CALL_MERGE)
+
+
+def test_union_mode_validation_and_workspace(S):
+    b = ctypes.c_size_t()
+    bad = S.params(seq_len=256, select_mode=2)
+    assert S.lib.selkv_workspace_size(ctypes.byref(bad), S.CALL_SELECT, 0, ctypes.byref(b)) == 1
+    per_head = S.params(seq_len=256)
+    union = S.params(seq_len=256, select_mode="union")
+    assert S.workspace_bytes(per_head, S.CALL_SELECT) == 0
+    assert S.workspace_bytes(union, S.CALL_SELECT) >= 4 * (256 - 16) * 2
+    assert S.workspace_bytes(union, S.CALL_BIAS) >= S.workspace_bytes(per_head, S.CALL_BIAS) + 4 * 8 * 64
+    assert S.workspace_bytes(union, S.CALL_MERGE) == S.workspace_bytes(per_head, S.CALL_MERGE)

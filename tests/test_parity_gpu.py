@@ -515,3 +515,131 @@ def test_full_cosine_deterministic_and_grouped_in_order(S):
         assert torch.equal(outs[0][k], outs[1][k]), k
     tg = outs[0]["target"].cpu().numpy()
     assert ((tg >= 0) & (tg < outs[0]["kept"].shape[2])).all()
+
+
+# ------------------------------------------------------------------ GQA union mode (Sec. 3.3, Sec. 3.6)
+UNION = [
+    dict(batch=1, H=2, G=2, d=64, n=512, W=32, dtype="fp32"),
+    dict(batch=2, H=4, G=2, d=128, n=700, W=16, dtype="bf16"),
+    dict(batch=1, H=8, G=4, d=128, n=2048, W=32, dtype="bf16"),
+    dict(batch=1, H=3, G=1, d=64, n=300, W=8, dtype="fp32", budget_ratio=0.05),        # m < m_r: recent only
+    dict(batch=1, H=2, G=2, d=64, n=400, W=32, dtype="bf16", route_mode="full_cosine"),
+    dict(batch=1, H=4, G=2, d=64, n=256, W=32, dtype="fp32", budget_ratio=1.0),         # nothing evicted
+]
+
+
+@pytest.mark.parametrize("case", UNION, ids=[f"union{i}" for i in range(len(UNION))])
+def test_gqa_union_select_merge_bias(S, case):
+    """Union selection fed the oracle's fp32 scores must match bit for bit
+    (the trim mean is fp32 in head order on both sides); merge and the
+    head-averaged bias are then checked per head against the oracle."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 3 + case["H"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"], device=DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case, select_mode="union", **kw)
+    tol = TOL[case["dtype"]]
+    B, H, n, d = K.shape
+    m, mr, ms = S.budget(p)
+    comp = S.Compressor(p, DEV)
+    S.score(p, K, V, Q, comp.score, comp.attn, comp.vnorm, comp.ws_score)
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(K), np64(V), np64(Q)
+    s_in, a_in, vn_in = comp.score.clone(), comp.attn.clone(), comp.vnorm.clone()
+    heads = {}
+    for b in range(B):
+        for h in range(H):
+            a, vn, sc = oracle_head_score(K64[b, h], V64[b, h], Q64[b, h * p.group:(h + 1) * p.group], p)
+            heads[(b, h)] = dict(a32=a.astype(np.float32).astype(np.float64), vn=vn,
+                                 s32=sc.astype(np.float32))
+            s_in[b, h] = torch.as_tensor(heads[(b, h)]["s32"])
+            a_in[b, h] = torch.as_tensor(heads[(b, h)]["a32"], dtype=torch.float32)
+            vn_in[b, h] = torch.as_tensor(vn, dtype=torch.float32)
+    S.select(p, s_in, comp.kept, comp.evicted, comp.ws_select)
+    torch.cuda.synchronize()
+    gate_mode = GATE[p.gate_mode]
+    alpha = float(np.float32(p.alpha))
+    t_in, g_in = comp.target.clone(), comp.gate.clone()
+    want_bias = {}
+    for b in range(B):
+        kept, ev = O.select_union(np.stack([heads[(b, h)]["s32"] for h in range(H)]), n, m, mr)
+        for h in range(H):
+            np.testing.assert_array_equal(comp.kept[b, h].cpu().numpy(), kept, err_msg=f"kept[{b},{h}]")
+            np.testing.assert_array_equal(comp.evicted[b, h].cpu().numpy(), ev, err_msg=f"evicted[{b},{h}]")
+        tgs, gs = [], []
+        for h in range(H):
+            hd = heads[(b, h)]
+            if p.route_mode == 1:
+                tg, _ = O.route_full_cosine(V64[b, h], kept, ev)
+            else:
+                tg = O.route_bucket(hd["a32"], kept, ev, p.bucket)
+            g = O.gate(V64[b, h], kept, ev, tg, gate_mode, float(np.float32(p.gate_threshold)),
+                       float(np.float32(p.gate_temperature)))
+            g32 = g.astype(np.float32).astype(np.float64)
+            tgs.append(tg)
+            gs.append(g32)
+            t_in[b, h] = torch.as_tensor(tg, dtype=torch.int32)
+            g_in[b, h] = torch.as_tensor(g32, dtype=torch.float32)
+        want_bias[b] = O.ratio_bias_union(np.stack([heads[(b, h)]["a32"] for h in range(H)]), kept, ev,
+                                          np.stack(tgs), np.stack(gs), alpha)
+    # merge with the shared set, per head (bucket routing only: full-cosine targets may near-tie)
+    if p.route_mode == 0:
+        S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
+                comp.ws_merge)
+        torch.cuda.synchronize()
+        for b in range(B):
+            kept = comp.kept[b, 0].cpu().numpy()
+            ev = comp.evicted[b, 0].cpu().numpy()
+            for h in range(H):
+                hd = heads[(b, h)]
+                np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), t_in[b, h].cpu().numpy())
+                _, v_out, _ = O.merge(K64[b, h], V64[b, h], hd["a32"], kept, ev, t_in[b, h].cpu().numpy(),
+                                      g_in[b, h].cpu().double().numpy())
+                assert_close_rows(np64(comp.V_out[b, h]), v_out, tol, f"V_out[{b},{h}]")
+    S.bias(p, a_in, comp.kept, comp.evicted, t_in, g_in, comp.bias, comp.ws_bias)
+    torch.cuda.synchronize()
+    for b in range(B):
+        for h in range(H):
+            err = np.abs(np64(comp.bias[b, h]) - want_bias[b]).max(initial=0)
+            assert err <= max(abs(alpha), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
+        assert all(torch.equal(comp.bias[b, 0], comp.bias[b, h]) for h in range(H))
+
+
+def test_gqa_union_end_to_end_llama_layer(S):
+    """The whole union-mode compression of a Llama-shaped layer on the GPU.
+    Checked by properties of the GPU's own scores (no oracle input comes from
+    the GPU): one kept set of m entries shared by the eight KV heads; every
+    kept candidate is among some head's top m_s; no union member that was
+    cut has a larger fp32 head-order mean (or an equal mean at a lower
+    position) than a kept one; the shared bias is finite and non-negative."""
+    w = synth.WORKLOADS["llama_layer"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w), select_mode="union")
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    m, mr, ms = S.budget(p)
+    n, H = p.seq_len, p.n_heads_kv
+    kept = comp.kept[0].cpu().numpy()
+    assert (kept == kept[0]).all(), "all KV heads share one kept set"
+    k0 = kept[0]
+    assert k0.shape[0] == m and (np.diff(k0) > 0).all() and (k0[ms:] == np.arange(n - mr, n)).all()
+    sc = comp.score[0].cpu().numpy()                       # [H, n - mr] fp32
+    pos = np.arange(n - mr)
+    picked = np.zeros(n - mr, dtype=bool)
+    for h in range(H):
+        order = np.lexsort((pos, -sc[h].astype(np.float64)))
+        picked[order[:ms]] = True
+    cand = k0[:ms]
+    assert picked[cand].all()
+    mean = np.zeros(n - mr, dtype=np.float32)
+    for h in range(H):
+        mean = (mean + sc[h]).astype(np.float32)
+    mean = (mean / np.float32(H)).astype(np.float64)
+    cut = np.flatnonzero(picked & ~np.isin(pos, cand))
+    worst_kept = min(zip(mean[cand], -cand))
+    best_cut = max(zip(mean[cut], -cut)) if cut.size else (-np.inf, 0)
+    assert worst_kept > best_cut
+    bias = comp.bias[0]
+    assert all(torch.equal(bias[0], bias[h]) for h in range(H))
+    assert torch.isfinite(bias).all() and (bias >= 0).all()
