@@ -36,7 +36,11 @@ Readings taken where the paper is silent or garbled:
     the union never falls short, so the shared kept set has exactly m
     entries.  The mean is taken in float32 in head order because it decides
     integers (which tokens survive) and the GPU decides in float32.  R is
-    averaged across KV heads and alpha * ln(mean R) is shared by them.
+    averaged across KV heads and alpha * ln(mean R) is shared by them;
+  * RoPE repositioning (Sec. 3.6 last subsection, Eq. 7; off by default):
+    the rotate-half convention (dimension j pairs with j + d/2, frequency
+    theta^(-2j/d)), retained key i moves from its position p_old = i to
+    p_new = its slot in the compressed cache (0 .. m-1, contiguous).
 """
 from __future__ import annotations
 
@@ -349,6 +353,32 @@ def ratio_bias_union(a_heads: np.ndarray, kept: np.ndarray, evicted: np.ndarray,
         a_kept = a[kept]
         R[h] = (a_kept + absorbed) / a_kept
     return alpha * np.log(R.mean(axis=0))
+
+
+# --------------------------------------------------------------------------
+# RoPE repositioning (Eq. 7)
+# --------------------------------------------------------------------------
+def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
+    """Rotary position embedding of rows x [r, d] at positions pos [r]
+    (negative positions rotate backwards, so rope(x, -p) is RoPE^-1 at p).
+    Dimension j < d/2 pairs with j + d/2 and turns by pos * theta^(-2j/d)."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    inv_freq = float(theta) ** (-2.0 * np.arange(half, dtype=np.float64) / d)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    x1, x2 = x[:, :half], x[:, half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=1)
+
+
+def reposition_keys(k_kept: np.ndarray, kept: np.ndarray, theta: float) -> np.ndarray:
+    """Eq. 7: k~_i = RoPE(RoPE^-1(k_i, p_old), p_new) with p_old the original
+    position of kept token i and p_new its contiguous slot in the compressed
+    cache.  k_kept [m, d] rows in slot order; kept [m] original positions."""
+    p_old = np.asarray(kept, dtype=np.float64)
+    p_new = np.arange(kept.shape[0], dtype=np.float64)
+    return rope(rope(k_kept, -p_old, theta), p_new, theta)
 
 
 # --------------------------------------------------------------------------

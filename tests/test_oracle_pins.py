@@ -469,3 +469,30 @@ def test_union_ratio_bias_single_head_is_per_head():
     g = rng.random(ev.shape[0])
     one = O.ratio_bias_union(a[None], kept, ev, tg[None], g[None], 0.5)
     assert np.allclose(one, O.ratio_bias(a, kept, ev, tg, g, 0.5), rtol=1e-14, atol=1e-15)
+
+
+# ------------------------------------------------------------------ RoPE repositioning (Eq. 7)
+def test_rope_reposition_hand_worked():
+    c = GOLD["rope_reposition"]
+    got = O.reposition_keys(np.array([[0.0] * 4] * 2 + [c["k"]]), np.array([0, 1, c["p_old"]]), c["theta"])
+    assert np.allclose(got[2], c["expected"], rtol=0, atol=1e-14)
+    assert np.allclose(got[:2], 0.0)
+
+
+def test_rope_properties():
+    rng = np.random.default_rng(9)
+    d, r = 64, 12
+    x = rng.standard_normal((r, d))
+    pos = rng.integers(0, 100000, size=r).astype(np.float64)
+    for theta in (10000.0, 500000.0):
+        y = O.rope(x, pos, theta)
+        assert np.allclose(np.linalg.norm(y, axis=1), np.linalg.norm(x, axis=1), rtol=1e-12)   # rotations
+        assert np.allclose(O.rope(y, -pos, theta), x, atol=1e-9)                              # inverse
+        # relative position: <rope(q, a), rope(k, b)> depends on a - b only
+        q, k = rng.standard_normal((1, d)), rng.standard_normal((1, d))
+        l1 = float((O.rope(q, np.array([900.0]), theta) @ O.rope(k, np.array([400.0]), theta).T)[0, 0])
+        l2 = float((O.rope(q, np.array([510.0]), theta) @ O.rope(k, np.array([10.0]), theta).T)[0, 0])
+        assert abs(l1 - l2) < 1e-9
+    # repositioning a key already at its slot changes nothing
+    ks = rng.standard_normal((5, d))
+    assert np.allclose(O.reposition_keys(ks, np.arange(5), 10000.0), ks, atol=1e-12)
