@@ -295,6 +295,26 @@ def measure_union(job, reps=3):
             "note": "select_mode union: per-KV-head top-m_s, union per layer, trim by mean score; R averaged over KV heads"}
 
 
+def measure_rope(job, theta=500000.0, reps=3):
+    """RoPE repositioning (Eq. 7) of the whole model's compressed keys, in
+    place on the job's K_out (run after the decode measurements).  Moves
+    each retained key once: read + write of B x H_kv x m x d elements."""
+    torch, selkv, w = job.torch, job.selkv, job.w
+    c = job.comp
+    job.selkv.rope_reposition(job.p, c.kept, c.K_out, theta)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        selkv.rope_reposition(job.p, c.kept, c.K_out, theta)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = 2 * c.K_out.numel() * c.K_out.element_size() + c.kept.numel() * 4
+    return {"ms": round(ms, 4), "alg_bytes": nbytes, "achieved_GBs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "rope_theta": theta}
+
+
 def measure_full_cosine(job, layers, reps=3):
     """The all-pairs cosine routing variant of the merge call on the first
     `layers` layers of the resident workload, fed the compressed job's own
@@ -399,6 +419,7 @@ def main():
         out["full_cosine_routing"] = measure_full_cosine(job, min(args.full_cosine_layers, w.layers))
     if not args.no_union:
         out["gqa_union"] = measure_union(job)
+    out["rope_reposition"] = measure_rope(job)
 
     traffic = read_traffic()
     out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),

@@ -226,6 +226,22 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
                                   const int32_t* evicted_idx, const int32_t* target, const float* gate,
                                   float* bias, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Step 7 of Algorithm 1: RoPE repositioning (Sec. 3.6 last subsection,
+ * Eq. 7; the paper leaves it off for long contexts).
+ *
+ * K~_s = RoPE(RoPE^-1(K_out[s], kept_idx[s]), s): the key in kept slot s
+ * moves from its original position to the contiguous position s.  RoPE is
+ * the rotate-half form: dimension j < d/2 pairs with j + d/2 and turns by
+ * position * rope_theta^(-2j/d).  The two rotations are applied as one turn
+ * by (s - kept_idx[s]) * rope_theta^(-2j/d), formed and reduced in fp64;
+ * rows already at their slot are left bit for bit.
+ * In:  kept_idx [B, H_kv, m] (from selkv_select); rope_theta > 1 (10000 for
+ *      Llama 2, 500000 for Llama 3).
+ * In/out: K_out [B, H_kv, m, d] (kv_dtype, from selkv_merge), rewritten in place.
+ * Workspace: none. */
+SELKV_API selkv_status selkv_rope_reposition(const selkv_params* p, const int32_t* kept_idx, void* K_out,
+                                             double rope_theta, hipStream_t stream);
+
 /* Decode with the compressed cache (Sec. 3.1 last paragraph, Algorithm 1
  * "Decode with compressed cache + alpha log R bias").
  *

@@ -83,6 +83,8 @@ hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, con
 hipError_t launch_union_select(const Shape& s, const UnionPlan& p, const float* score, int32_t* kept,
                                int32_t* evicted, void* ws, hipStream_t st);
 hipError_t launch_union_bias(const Shape& s, const float* r1, float* bias, float alpha, hipStream_t st);
+hipError_t launch_rope_reposition(const Shape& s, int dtype, const int32_t* kept, void* K_out, double theta,
+                                  hipStream_t st);
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int d, int G, int dtype, float scale,
                          const DecodePlan& plan, const void* q, const void* K, const void* V, const float* bias,
                          float* out, void* ws, hipStream_t st);

@@ -241,6 +241,17 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
   return hip_status(launch_union_bias(s, dst, bias, p->alpha, stream));
 }
 
+SELKV_API selkv_status selkv_rope_reposition(const selkv_params* p, const int32_t* kept_idx, void* K_out,
+                                             double rope_theta, hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if (!kept_idx || !K_out) return SELKV_EINVAL;
+  if (!(rope_theta > 1.0) || !isfinite(rope_theta)) return SELKV_EINVAL;
+  if (!aligned(kept_idx, 4) || !aligned(K_out, 16)) return SELKV_EALIGN;
+  return hip_status(launch_rope_reposition(s, p->kv_dtype, kept_idx, K_out, rope_theta, stream));
+}
+
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream) {

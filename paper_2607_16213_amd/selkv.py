@@ -74,6 +74,7 @@ def _load():
         "selkv_merge": (ctypes.c_int, [P, vp, vp, fp, fp, ip, ip, vp, vp, ip, fp, vp, sz, vp]),
         "selkv_bias": (ctypes.c_int, [P, fp, ip, ip, ip, fp, fp, vp, sz, vp]),
         "selkv_decode_attn": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp, sz, vp]),
+        "selkv_rope_reposition": (ctypes.c_int, [P, ip, vp, ctypes.c_double, vp]),
         "selkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "selkv_abi_version": (ctypes.c_int32, []),
     }
@@ -202,6 +203,15 @@ def bias(p, attn, kept, evicted, target, gate, bias_out, ws, stream=None):
     _check(lib.selkv_bias(ctypes.byref(p), _ptr(attn), _ptr(kept), _ptr(evicted), _ptr(target), _ptr(gate),
                           _ptr(bias_out), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
            "selkv_bias")
+
+
+def rope_reposition(p, kept, K_out, rope_theta, stream=None):
+    B, H, d = p.batch, p.n_heads_kv, p.head_dim
+    m, mr, ms = budget(p)
+    _dev(kept, (B, H, m), torch.int32, "kept_idx")
+    _dev(K_out, (B, H, m, d), _kvdt(p), "K_out")
+    _check(lib.selkv_rope_reposition(ctypes.byref(p), _ptr(kept), _ptr(K_out), float(rope_theta), _stream(stream)),
+           "selkv_rope_reposition")
 
 
 def decode_attn(p, q, K, V, bias_in, out, ws, stream=None):

@@ -136,3 +136,14 @@ def test_union_mode_validation_and_workspace(S):
     assert S.workspace_bytes(union, S.CALL_SELECT) >= 4 * (256 - 16) * 2
     assert S.workspace_bytes(union, S.CALL_BIAS) >= S.workspace_bytes(per_head, S.CALL_BIAS) + 4 * 8 * 64
     assert S.workspace_bytes(union, S.CALL_MERGE) == S.workspace_bytes(per_head, S.CALL_MERGE)
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_rope_reposition_validation(S):
+    p = S.params(seq_len=256)
+    fake, mis = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10004)
+    f = S.lib.selkv_rope_reposition
+    assert f(ctypes.byref(p), fake, fake, 1.0, None) == 1          # theta must exceed 1
+    assert f(ctypes.byref(p), fake, fake, float("nan"), None) == 1
+    assert f(ctypes.byref(p), None, fake, 10000.0, None) == 1
+    assert f(ctypes.byref(p), fake, mis, 10000.0, None) == 4       # K_out 16-byte aligned

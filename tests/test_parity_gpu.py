@@ -643,3 +643,45 @@ def test_gqa_union_end_to_end_llama_layer(S):
     bias = comp.bias[0]
     assert all(torch.equal(bias[0], bias[h]) for h in range(H))
     assert torch.isfinite(bias).all() and (bias >= 0).all()
+
+
+# ------------------------------------------------------------------ RoPE repositioning (Eq. 7)
+ROPE = [
+    dict(batch=1, H=2, d=64, n=512, dtype="fp32", theta=10000.0),
+    dict(batch=2, H=2, d=128, n=3000, dtype="bf16", theta=500000.0),
+    dict(batch=1, H=1, d=128, n=20000, dtype="fp32", theta=10000.0),       # angles up to 1.5e4 rad
+    dict(batch=1, H=2, d=64, n=700, dtype="bf16", theta=10000.0, budget_ratio=1.0),
+]
+
+
+@pytest.mark.parametrize("case", ROPE, ids=[f"rope{i}" for i in range(len(ROPE))])
+def test_rope_reposition(S, case):
+    """Eq. 7 on the GPU against the oracle's two rotations, for kept sets
+    spread over the whole sequence; rows already at their slot stay bit for
+    bit (a full budget keeps every key where it was)."""
+    B, H, d, n = case["batch"], case["H"], case["d"], case["n"]
+    dt = torch.bfloat16 if case["dtype"] == "bf16" else torch.float32
+    p = S.params(batch=B, n_heads_kv=H, group=1, head_dim=d, seq_len=n, window=8, kv_dtype=case["dtype"],
+                 budget_ratio=case.get("budget_ratio", 0.25))
+    m, mr, ms = S.budget(p)
+    g = torch.Generator().manual_seed(n + d)
+    K = torch.randn((B, H, n, d), generator=g).to(dt)
+    kept = torch.empty((B, H, m), dtype=torch.int32)
+    for b in range(B):
+        for h in range(H):
+            kept[b, h] = torch.sort(torch.randperm(n, generator=g)[:m]).values.to(torch.int32)
+    K_out = torch.gather(K, 2, kept.long()[..., None].expand(B, H, m, d)).contiguous()
+    kd, Kd = kept.to(DEV), K_out.to(DEV)
+    S.rope_reposition(p, kd, Kd, case["theta"])
+    torch.cuda.synchronize()
+    got = Kd.cpu()
+    tol = TOL[case["dtype"]]
+    for b in range(B):
+        for h in range(H):
+            ks = kept[b, h].numpy()
+            want = O.reposition_keys(K_out[b, h].double().numpy(), ks, case["theta"])
+            assert_close_rows(got[b, h].double().numpy(), want, tol, f"K~[{b},{h}]")
+            same = ks == np.arange(m)
+            assert torch.equal(got[b, h][torch.as_tensor(same)], K_out[b, h][torch.as_tensor(same)])
+    if case.get("budget_ratio") == 1.0:
+        assert torch.equal(got, K_out)
