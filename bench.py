@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--print-source-hash", action="store_true", help="print the decode source hash and exit")
     ap.add_argument("--full-cosine-layers", type=int, default=1,
                     help="layers timed with the all-pairs cosine routing variant (0 = skip)")
+    ap.add_argument("--no-generation", action="store_true", help="skip the growing-cache generation loop timing")
     ap.add_argument("--no-union", action="store_true", help="skip the GQA union-mode compression timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
@@ -295,6 +296,60 @@ def measure_union(job, reps=3):
             "note": "select_mode union: per-KV-head top-m_s, union per layer, trim by mean score; R averaged over KV heads"}
 
 
+def measure_generation(job, steps=64, reps=3):
+    """The decode loop after compression with growing caches: every step
+    appends one token's key and value (bias 0) to each layer's compressed
+    cache and attends over it (selkv_decode_append), all layers in order,
+    captured once into a HIP graph.  Reports microseconds per generated
+    token (all layers) and per layer-step."""
+    torch, selkv, w = job.torch, job.selkv, job.w
+    c, dev = job.comp, job.K.device
+    L, B, H, G, d = w.layers, w.batch, w.n_heads_kv, w.group, w.head_dim
+    m, cap = job.m, job.m + steps
+    Kg = torch.zeros((L, B, H, cap, d), dtype=job.K.dtype, device=dev)
+    Vg = torch.zeros_like(Kg)
+    bg = torch.zeros((L, B, H, cap), dtype=torch.float32, device=dev)
+    Kg[..., :m, :] = c.K_out.view(L, B, H, m, d)
+    Vg[..., :m, :] = c.V_out.view(L, B, H, m, d)
+    bg[..., :m] = c.bias.view(L, B, H, m)
+    gen = torch.Generator(device=dev).manual_seed(4242)
+    kn = torch.randn((steps, L, B, H, d), generator=gen, device=dev).to(job.K.dtype)
+    vn = torch.randn((steps, L, B, H, d), generator=gen, device=dev).to(job.K.dtype)
+    qs = job.Qd[:steps] if job.T >= steps else job.Qd[torch.arange(steps) % job.T]
+    ws = selkv.workspace(job.pd, selkv.CALL_DECODE, dev, cap)
+    outs = torch.empty((L, B, H * G, d), dtype=torch.float32, device=dev)
+
+    def loop():
+        for t in range(steps):
+            for layer in range(L):
+                selkv.decode_append(job.pd, qs[t, layer], kn[t, layer], vn[t, layer], Kg[layer], Vg[layer],
+                                    bg[layer], m + t, outs[layer], ws)
+
+    loop()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        loop()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        loop()
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    per_token_us = e0.elapsed_time(e1) * 1e3 / (reps * steps)
+    del Kg, Vg, bg, graph
+    return {"steps": steps, "us_per_token": round(per_token_us, 2), "us_per_layer_step": round(per_token_us / L, 3),
+            "note": "append + biased decode per layer (bias 0 on appended tokens), caches m..m+steps-1 entries"}
+
+
 def measure_rope(job, theta=500000.0, reps=3):
     """RoPE repositioning (Eq. 7) of the whole model's compressed keys, in
     place on the job's K_out (run after the decode measurements).  Moves
@@ -415,6 +470,8 @@ def main():
         out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
         out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
 
+    if not args.no_generation:
+        out["generation_loop"] = measure_generation(job)
     if args.full_cosine_layers > 0:
         out["full_cosine_routing"] = measure_full_cosine(job, min(args.full_cosine_layers, w.layers))
     if not args.no_union:

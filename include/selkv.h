@@ -261,6 +261,23 @@ SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, c
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream);
 
+/* One generation step over a cache that grows (the decode loop after
+ * compression, Sec. 4.4): the new token's key and value are written at
+ * entry cache_len of every KV head, with bias 0 there when bias is given
+ * (a new token absorbed nothing, so R = 1), and then the step attends over
+ * the cache_len + 1 entries exactly as selkv_decode_attn.
+ * In:  q [B, H_kv*G, d]; k_new, v_new [B, H_kv, d] (kv_dtype);
+ *      0 <= cache_len < capacity.
+ * In/out: K, V [B, H_kv, capacity, d] (entries past cache_len + 1 are not
+ *      read); bias [B, H_kv, capacity] fp32 or NULL.
+ * Out: out [B, H_kv*G, d] fp32.
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_DECODE, capacity) covers every
+ *      cache_len below capacity. */
+SELKV_API selkv_status selkv_decode_append(const selkv_params* p, const void* q, const void* k_new,
+                                           const void* v_new, void* K, void* V, float* bias, int32_t cache_len,
+                                           int32_t capacity, float* out, void* ws, size_t ws_bytes,
+                                           hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 SELKV_API const char* selkv_status_string(selkv_status s);
 

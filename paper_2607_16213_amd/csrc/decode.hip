@@ -124,6 +124,7 @@ struct DecodeArgs {
   float* part_o;    // [heads, nsplit, G, D]
   float2* part_ml;  // [heads, nsplit, G]: running max (log2 domain) and sum
   int L, chunk, nsplit;
+  int stride;       // entries between consecutive heads in K, V and bias (>= L)
   float c2;         // scale * log2(e)
 };
 
@@ -136,9 +137,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int L = a.L;
-  const char* Kh = a.K + (size_t)head * L * RB;
-  const char* Vh = a.V + (size_t)head * L * RB;
-  const float* bh = BIAS ? a.bias + (size_t)head * L : nullptr;
+  const char* Kh = a.K + (size_t)head * a.stride * RB;
+  const char* Vh = a.V + (size_t)head * a.stride * RB;
+  const float* bh = BIAS ? a.bias + (size_t)head * a.stride : nullptr;
 
   float q[G][E];
 #pragma unroll
@@ -337,9 +338,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int L = a.L;
-  const char* Kh = a.K + (size_t)head * L * RB;
-  const char* Vh = a.V + (size_t)head * L * RB;
-  const float* bh = BIAS ? a.bias + (size_t)head * L : nullptr;
+  const char* Kh = a.K + (size_t)head * a.stride * RB;
+  const char* Vh = a.V + (size_t)head * a.stride * RB;
+  const float* bh = BIAS ? a.bias + (size_t)head * a.stride : nullptr;
 
   // Q as the MFMA A operand: lane (c, r) holds chunks 4j + r of query row c
   Chunk16 qf[NCH];
@@ -526,7 +527,30 @@ hipError_t launch_td(int64_t heads, int G, const DecodePlan& p, DecodeArgs& a, h
   }
 }
 
+// Writes the new token's key and value rows at entry `len` of every head's
+// cache and a zero bias there (new tokens absorbed nothing: R = 1).
+__global__ __launch_bounds__(64) void decode_append_kernel(const char* k_new, const char* v_new, char* K, char* V,
+                                                           float* bias, int len, int stride, int row_bytes) {
+  const int64_t head = blockIdx.x;
+  char* kd = K + ((size_t)head * stride + len) * row_bytes;
+  char* vd = V + ((size_t)head * stride + len) * row_bytes;
+  for (int c = threadIdx.x; c * 16 < row_bytes; c += 64) {
+    store16(kd + c * 16, load16(k_new + (size_t)head * row_bytes + c * 16));
+    store16(vd + c * 16, load16(v_new + (size_t)head * row_bytes + c * 16));
+  }
+  if (bias && threadIdx.x == 0) bias[(size_t)head * stride + len] = 0.f;
+}
+
 }  // namespace
+
+hipError_t launch_decode_append(int64_t heads, int len, int stride, int d, int dtype, const void* k_new,
+                                const void* v_new, void* K, void* V, float* bias, hipStream_t st) {
+  const int row_bytes = d * (dtype == SELKV_BF16 ? 2 : 4);
+  hipLaunchKernelGGL(decode_append_kernel, dim3((unsigned)heads), dim3(64), 0, st,
+                     static_cast<const char*>(k_new), static_cast<const char*>(v_new), static_cast<char*>(K),
+                     static_cast<char*>(V), bias, len, stride, row_bytes);
+  return hipGetLastError();
+}
 
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
   DecodePlan p{};
@@ -545,11 +569,12 @@ DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
   return p;
 }
 
-hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int d, int G, int dtype, float scale,
-                         const DecodePlan& p, const void* q, const void* K, const void* V, const float* bias,
-                         float* out, void* ws, hipStream_t st) {
+hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int stride, int d, int G, int dtype,
+                         float scale, const DecodePlan& p, const void* q, const void* K, const void* V,
+                         const float* bias, float* out, void* ws, hipStream_t st) {
   (void)n_heads_kv;
   DecodeArgs a{};
+  a.stride = stride;
   a.q = static_cast<const char*>(q);
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);

@@ -269,8 +269,35 @@ SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, c
   const DecodePlan plan = plan_decode(heads, cache_len, p->head_dim, p->group);
   selkv_status st = check_ws(ws, ws_bytes, plan.bytes);
   if (st != SELKV_OK) return st;
-  return hip_status(launch_decode(heads, p->n_heads_kv, cache_len, p->head_dim, p->group, p->kv_dtype,
+  return hip_status(launch_decode(heads, p->n_heads_kv, cache_len, cache_len, p->head_dim, p->group, p->kv_dtype,
                                   eff_scale(p), plan, q, K, V, bias, out, ws, stream));
+}
+
+SELKV_API selkv_status selkv_decode_append(const selkv_params* p, const void* q, const void* k_new,
+                                           const void* v_new, void* K, void* V, float* bias, int32_t cache_len,
+                                           int32_t capacity, float* out, void* ws, size_t ws_bytes,
+                                           hipStream_t stream) {
+  if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
+  if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
+  if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || cache_len < 0 || capacity < 1) return SELKV_EINVAL;
+  if (cache_len >= capacity) return SELKV_EINVAL;                 // no room for the new entry
+  if (p->group > 8) return SELKV_EUNSUPPORTED;
+  if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+  if (!(p->scale >= 0.f) || !isfinite(p->scale)) return SELKV_EINVAL;
+  const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
+  if (heads > 65535) return SELKV_EUNSUPPORTED;
+  if (!q || !k_new || !v_new || !K || !V || !out) return SELKV_EINVAL;
+  if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(K, 16) || !aligned(V, 16) ||
+      !aligned(bias, 4) || !aligned(out, 16))
+    return SELKV_EALIGN;
+  const DecodePlan plan = plan_decode(heads, cache_len + 1, p->head_dim, p->group);
+  selkv_status st = check_ws(ws, ws_bytes, plan.bytes);
+  if (st != SELKV_OK) return st;
+  hipError_t e = launch_decode_append(heads, cache_len, capacity, p->head_dim, p->kv_dtype, k_new, v_new, K, V,
+                                      bias, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  return hip_status(launch_decode(heads, p->n_heads_kv, cache_len + 1, capacity, p->head_dim, p->group,
+                                  p->kv_dtype, eff_scale(p), plan, q, K, V, bias, out, ws, stream));
 }
 
 SELKV_API const char* selkv_status_string(selkv_status s) {

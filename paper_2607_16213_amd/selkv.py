@@ -75,6 +75,7 @@ def _load():
         "selkv_bias": (ctypes.c_int, [P, fp, ip, ip, ip, fp, fp, vp, sz, vp]),
         "selkv_decode_attn": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp, sz, vp]),
         "selkv_rope_reposition": (ctypes.c_int, [P, ip, vp, ctypes.c_double, vp]),
+        "selkv_decode_append": (ctypes.c_int, [P, vp, vp, vp, vp, vp, fp, i32, i32, fp, vp, sz, vp]),
         "selkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "selkv_abi_version": (ctypes.c_int32, []),
     }
@@ -225,6 +226,23 @@ def decode_attn(p, q, K, V, bias_in, out, ws, stream=None):
     _dev(out, (B, H * p.group, d), torch.float32, "out")
     _check(lib.selkv_decode_attn(ctypes.byref(p), _ptr(q), _ptr(K), _ptr(V), _ptr(bias_in), L, _ptr(out), _ptr(ws),
                                  ws.numel() if ws is not None else 0, _stream(stream)), "selkv_decode_attn")
+
+
+def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=None):
+    """Append (k_new, v_new) at entry cache_len (bias 0 there) and attend over
+    cache_len + 1 entries; K, V [B, H, capacity, d] and bias [B, H, capacity]."""
+    B, H, d = p.batch, p.n_heads_kv, p.head_dim
+    cap = K.shape[2]
+    dt = _kvdt(p)
+    _dev(q, (B, H * p.group, d), dt, "q")
+    _dev(k_new, (B, H, d), dt, "k_new"); _dev(v_new, (B, H, d), dt, "v_new")
+    _dev(K, (B, H, cap, d), dt, "K"); _dev(V, (B, H, cap, d), dt, "V")
+    if bias_io is not None:
+        _dev(bias_io, (B, H, cap), torch.float32, "bias")
+    _dev(out, (B, H * p.group, d), torch.float32, "out")
+    _check(lib.selkv_decode_append(ctypes.byref(p), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(K), _ptr(V),
+                                   _ptr(bias_io), int(cache_len), cap, _ptr(out), _ptr(ws),
+                                   ws.numel() if ws is not None else 0, _stream(stream)), "selkv_decode_append")
 
 
 class Compressor:

@@ -147,3 +147,15 @@ def test_rope_reposition_validation(S):
     assert f(ctypes.byref(p), fake, fake, float("nan"), None) == 1
     assert f(ctypes.byref(p), None, fake, 10000.0, None) == 1
     assert f(ctypes.byref(p), fake, mis, 10000.0, None) == 4       # K_out 16-byte aligned
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_decode_append_validation(S):
+    p = S.params(seq_len=256)
+    fake = ctypes.c_void_p(0x10000)
+    f = S.lib.selkv_decode_append
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 8, 8, fake, fake, 1 << 30, None) == 1   # full
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, -1, 8, fake, fake, 1 << 30, None) == 1
+    assert f(ctypes.byref(p), fake, ctypes.c_void_p(0x10008), fake, fake, fake, fake, 3, 8, fake, fake, 1 << 30,
+             None) == 4
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 3, 8, fake, fake, 0, None) == 5

@@ -685,3 +685,53 @@ def test_rope_reposition(S, case):
             assert torch.equal(got[b, h][torch.as_tensor(same)], K_out[b, h][torch.as_tensor(same)])
     if case.get("budget_ratio") == 1.0:
         assert torch.equal(got, K_out)
+
+
+# ------------------------------------------------------------------ generation loop with appended tokens
+@pytest.mark.parametrize("name", ["tiny", "llama_layer"])
+def test_decode_with_appended_tokens(S, name):
+    """The decode loop after compression: each step appends the new token's
+    key and value (bias 0) to the compressed cache and attends over all of
+    it.  Checked against the oracle's decode over the compressed cache plus
+    the appended rows, at every step."""
+    w = synth.WORKLOADS[name]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w))
+    B, H, G, d = p.batch, p.n_heads_kv, p.group, p.head_dim
+    heads = [(0, 0)] if name == "tiny" else [(0, 0), (0, 5)]
+    # the compressed cache comes from the oracle (its outputs rounded to storage)
+    K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
+    m = S.budget(p)[0]
+    steps = 12
+    cap = m + steps
+    dt = t["K"].dtype
+    Kh = torch.zeros((B, H, cap, d), dtype=dt)
+    Vh = torch.zeros_like(Kh)
+    bh = torch.full((B, H, cap), 7.0, dtype=torch.float32)      # overwritten where appended
+    bh[:, :, :m] = 0.0
+    for (b, h) in heads:
+        ch = oracle_chain(K64[b, h], V64[b, h], Q64[b, h * G:(h + 1) * G], p, GATE[p.gate_mode])
+        Kh[b, h, :m] = torch.as_tensor(ch["k_out"]).to(dt)
+        Vh[b, h, :m] = torch.as_tensor(ch["v_out"]).to(dt)
+        bh[b, h, :m] = torch.as_tensor(ch["bias"]).to(torch.float32)
+    Kc, Vc, bias = Kh.to(DEV), Vh.to(DEV), bh.to(DEV)
+    ws = S.workspace(p, S.CALL_DECODE, DEV, cap)
+    out = torch.empty((B, H * G, d), dtype=torch.float32, device=DEV)
+    g = torch.Generator().manual_seed(77)
+    tol = TOL[dtype_name(t["K"])]
+    for step in range(steps):
+        q = torch.randn((B, H * G, d), generator=g).to(dt)
+        kn = torch.randn((B, H, d), generator=g).to(dt)
+        vn = torch.randn((B, H, d), generator=g).to(dt)
+        S.decode_append(p, q.to(DEV), kn.to(DEV), vn.to(DEV), Kc, Vc, bias, m + step, out, ws)
+        torch.cuda.synchronize()
+        L = m + step + 1
+        assert torch.equal(Kc[:, :, m + step].cpu(), kn) and torch.equal(Vc[:, :, m + step].cpu(), vn)
+        assert (bias[:, :, m + step] == 0).all()
+        Kh[:, :, m + step], Vh[:, :, m + step], bh[:, :, m + step] = kn, vn, 0.0
+        ref = O.decode_batched(np64(q), np64(Kh[:, :, :L]), np64(Vh[:, :, :L]), np64(bh[:, :, :L]), G,
+                               oracle_scale(p))
+        got = out.cpu().double().numpy()
+        for (b, h) in heads:
+            assert_close_rows(got[b, h * G:(h + 1) * G], ref[b, h * G:(h + 1) * G], tol, f"append step {step}")
+    assert torch.equal(bias.cpu(), bh)
