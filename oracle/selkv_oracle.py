@@ -40,7 +40,11 @@ Readings taken where the paper is silent or garbled:
   * RoPE repositioning (Sec. 3.6 last subsection, Eq. 7; off by default):
     the rotate-half convention (dimension j pairs with j + d/2, frequency
     theta^(-2j/d)), retained key i moves from its position p_old = i to
-    p_new = its slot in the compressed cache (0 .. m-1, contiguous).
+    p_new = its slot in the compressed cache (0 .. m-1, contiguous);
+  * alternative readings, as modes: route_bucket_nearest sends the evicted
+    tokens of a bucket that keeps nothing to the nearest kept position
+    instead of dropping them; merge(..., merge_keys=True) averages keys with
+    the value weights of Eq. 5.
 """
 from __future__ import annotations
 
@@ -228,6 +232,21 @@ def route_bucket(a: np.ndarray, kept: np.ndarray, evicted: np.ndarray, bucket: i
     return target
 
 
+def route_bucket_nearest(a: np.ndarray, kept: np.ndarray, evicted: np.ndarray, bucket: int) -> np.ndarray:
+    """Alternative reading of Eq. 3 for a bucket that keeps no token (the
+    paper is silent): instead of being dropped, each of its evicted tokens
+    goes to the kept token nearest to it by position (the lower position
+    when two are equally near).  Buckets that keep a token route as Eq. 3.
+    """
+    target = route_bucket(a, kept, evicted, bucket)
+    for e, j in enumerate(evicted):
+        if target[e] >= 0:
+            continue
+        dist = np.abs(kept.astype(np.int64) - int(j))
+        target[e] = int(np.flatnonzero(dist == dist.min())[0])     # kept is ascending: lowest position
+    return target
+
+
 def cosine(u: np.ndarray, v: np.ndarray) -> float:
     """Eq. 4: cosine similarity of two value vectors; 0 if either is zero."""
     nu = math.sqrt(float(np.dot(u, u)))
@@ -292,12 +311,14 @@ def gate(v: np.ndarray, kept: np.ndarray, evicted: np.ndarray, target: np.ndarra
 
 
 def merge(k: np.ndarray, v: np.ndarray, a: np.ndarray, kept: np.ndarray,
-          evicted: np.ndarray, target: np.ndarray, g: np.ndarray):
+          evicted: np.ndarray, target: np.ndarray, g: np.ndarray, merge_keys: bool = False):
     """Eq. 5: the merged value of kept token i is
 
         v~_i = (a_i v_i + sum_{pi(j)=i} g_j a_j v_j) / (a_i + sum_{pi(j)=i} g_j a_j)
 
-    with a the window-cumulative attention.  Keys are gathered unchanged.
+    with a the window-cumulative attention.  Keys are gathered unchanged
+    (Eq. 5 defines only values); merge_keys=True is the alternative reading
+    that applies the same weights to the keys.
     Returns (K~ [m, d], V~ [m, d], w [m]) where w_i is the denominator.
     """
     k = np.asarray(k, dtype=np.float64)
@@ -305,14 +326,17 @@ def merge(k: np.ndarray, v: np.ndarray, a: np.ndarray, kept: np.ndarray,
     a_kept = a[kept]
     assert (a_kept > 1e-30).all(), "a kept token with no window attention is outside the contract"
     num = a_kept[:, None] * v[kept]
+    knum = a_kept[:, None] * k[kept]
     den = a_kept.copy()
     for e, j in enumerate(evicted):
         t = int(target[e])
         if t < 0:
             continue
         num[t] += g[e] * a[j] * v[j]
+        knum[t] += g[e] * a[j] * k[j]
         den[t] += g[e] * a[j]
-    return k[kept].copy(), num / den[:, None], den
+    k_out = knum / den[:, None] if merge_keys else k[kept].copy()
+    return k_out, num / den[:, None], den
 
 
 # --------------------------------------------------------------------------

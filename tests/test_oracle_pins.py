@@ -496,3 +496,35 @@ def test_rope_properties():
     # repositioning a key already at its slot changes nothing
     ks = rng.standard_normal((5, d))
     assert np.allclose(O.reposition_keys(ks, np.arange(5), 10000.0), ks, atol=1e-12)
+
+
+# ------------------------------------------------------------------ alternative readings (modes)
+def test_nearest_fallback_hand_worked():
+    c = GOLD["nearest_fallback"]
+    a, kept, ev = np.array(c["a"]), np.array(c["kept"]), np.array(c["evicted"])
+    assert O.route_bucket(a, kept, ev, c["bucket"]).tolist() == c["target_bucket"]
+    assert O.route_bucket_nearest(a, kept, ev, c["bucket"]).tolist() == c["target_nearest"]
+
+
+def test_nearest_fallback_tie_goes_low():
+    # evicted 5 sits 2 from kept 3 and 2 from kept 7: the lower position wins
+    a = np.ones(12)
+    kept, ev = np.array([3, 7]), np.array([0, 1, 2, 4, 5, 6, 8, 9, 10, 11])
+    t = O.route_bucket_nearest(a, kept, ev, 1)      # bucket 1: every evicted bucket is empty
+    assert t[ev.tolist().index(5)] == 0 and t[ev.tolist().index(6)] == 1 and t[ev.tolist().index(4)] == 0
+
+
+def test_merge_keys_closed_form():
+    """merge_keys applies Eq. 5's weights to keys: two tokens, one absorbed."""
+    k = np.array([[1.0, 0.0], [0.0, 2.0]])
+    v = np.array([[3.0, 1.0], [1.0, 1.0]])
+    a = np.array([0.75, 0.25])
+    kept, ev, tg, g = np.array([0]), np.array([1]), np.array([0]), np.array([0.5])
+    k_out, v_out, w = O.merge(k, v, a, kept, ev, tg, g, merge_keys=True)
+    # weights: a0 = 0.75, g1 a1 = 0.125, denominator 0.875
+    assert np.allclose(k_out[0], [0.75 / 0.875, 0.25 / 0.875]) and np.allclose(v_out[0], [2.375 / 0.875, 1.0])
+    k_plain, v_plain, _ = O.merge(k, v, a, kept, ev, tg, g)
+    assert np.array_equal(k_plain[0], k[0]) and np.allclose(v_plain, v_out)
+    # nothing absorbed: keys stay the kept keys either way
+    k_none, _, _ = O.merge(k, v, a, kept, ev, np.array([-1]), g, merge_keys=True)
+    assert np.array_equal(k_none[0], k[0])
