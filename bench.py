@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--full-cosine-layers", type=int, default=1,
                     help="layers timed with the all-pairs cosine routing variant (0 = skip)")
     ap.add_argument("--no-generation", action="store_true", help="skip the growing-cache generation loop timing")
-    ap.add_argument("--no-union", action="store_true", help="skip the GQA union-mode compression timing")
+    ap.add_argument("--no-union", action="store_true",
+                    help="skip the timings of the alternative modes (GQA union, nearest-kept fallback, merged keys)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
     return ap.parse_args()
@@ -255,17 +256,17 @@ def measure(job, steps, warmup):
     return wall, st
 
 
-def measure_union(job, reps=3):
-    """The GQA union mode of Sec. 3.3 / 3.6 (the paper's default for GQA
-    models) on the same resident cache: the four compression calls with one
-    kept set shared by the KV heads of each layer and the ratio averaged
-    across them.  Reuses the job's output buffers (run after the decode
-    measurements)."""
+def measure_variant(job, note, reps=3, **modes):
+    """One alternative mode of the compression on the same resident cache:
+    the four calls with `modes` set in the parameters (GQA union selection,
+    nearest-kept fallback, key merging, ...), each with its own workspaces.
+    Reuses the job's output buffers (run after the decode measurements)."""
     torch, selkv, w = job.torch, job.selkv, job.w
     p = selkv.params(batch=job.LB, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim, seq_len=w.seq_len,
-                     window=w.window, kv_dtype=w.dtype, budget_ratio=w.budgets[0], select_mode="union")
+                     window=w.window, kv_dtype=w.dtype, budget_ratio=w.budgets[0], **modes)
     c, dev = job.comp, job.K.device
     ws_sel = selkv.workspace(p, selkv.CALL_SELECT, dev)
+    ws_merge = selkv.workspace(p, selkv.CALL_MERGE, dev)
     ws_bias = selkv.workspace(p, selkv.CALL_BIAS, dev)
 
     def run(ev=None):
@@ -275,7 +276,7 @@ def measure_union(job, reps=3):
         selkv.select(p, c.score, c.kept, c.evicted, ws_sel)
         if ev: ev[2].record()
         selkv.merge(p, job.Kf, job.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
-                    c.ws_merge)
+                    ws_merge)
         if ev: ev[3].record()
         selkv.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, ws_bias)
         if ev: ev[4].record()
@@ -292,8 +293,24 @@ def measure_union(job, reps=3):
             tot[k] += ev[i].elapsed_time(ev[i + 1]) / reps
     comp_ms = sum(tot.values())
     return {"compress_ms": round(comp_ms, 4), "compress_tokens_per_s": round(w.seq_len * w.batch / (comp_ms / 1e3), 1),
-            "stages_ms": {k: round(v, 4) for k, v in tot.items()},
-            "note": "select_mode union: per-KV-head top-m_s, union per layer, trim by mean score; R averaged over KV heads"}
+            "stages_ms": {k: round(v, 4) for k, v in tot.items()}, "note": note}
+
+
+def measure_union(job):
+    """The GQA union mode of Sec. 3.3 / 3.6 (the paper's default for GQA
+    models): one kept set shared by the KV heads of each layer and the
+    ratio averaged across them."""
+    return measure_variant(job, "select_mode union: per-KV-head top-m_s, union per layer, trim by mean score; "
+                                "R averaged over KV heads", select_mode="union")
+
+
+def measure_readings(job):
+    """The alternative readings offered as modes: the nearest-kept fallback
+    for buckets that keep no token, and keys merged with the value weights."""
+    return {"bucket_nearest": measure_variant(job, "route_mode bucket_nearest: empty buckets route to the nearest "
+                                                   "kept token, absorbed by the neighbouring buckets' waves",
+                                              route_mode="bucket_nearest"),
+            "merge_keys": measure_variant(job, "merge_keys 1: keys merged with the Eq. 5 weights", merge_keys=1)}
 
 
 def measure_generation(job, steps=64, reps=3):
@@ -476,6 +493,7 @@ def main():
         out["full_cosine_routing"] = measure_full_cosine(job, min(args.full_cosine_layers, w.layers))
     if not args.no_union:
         out["gqa_union"] = measure_union(job)
+        out["alt_readings"] = measure_readings(job)
     out["rope_reposition"] = measure_rope(job)
 
     traffic = read_traffic()

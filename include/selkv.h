@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define SELKV_ABI_VERSION 2
+#define SELKV_ABI_VERSION 3
 
 typedef enum selkv_status {
   SELKV_OK = 0,
@@ -72,10 +72,15 @@ typedef enum selkv_gate_mode {
 } selkv_gate_mode;
 
 /* Merge-target routing of Sec. 3.4.  BUCKET is Eq. 3 (bucket-attention
- * routing); FULL_COSINE is the all-pairs cosine routing that Eq. 3 replaces. */
+ * routing; the evicted tokens of a bucket that keeps nothing are dropped);
+ * FULL_COSINE is the all-pairs cosine routing that Eq. 3 replaces;
+ * BUCKET_NEAREST is Eq. 3 with the other reading of the empty-bucket case
+ * the paper leaves open: those tokens go to the kept token nearest by
+ * position (the lower position when two are equally near). */
 typedef enum selkv_route_mode {
   SELKV_ROUTE_BUCKET = 0,
-  SELKV_ROUTE_FULL_COSINE = 1
+  SELKV_ROUTE_FULL_COSINE = 1,
+  SELKV_ROUTE_BUCKET_NEAREST = 2
 } selkv_route_mode;
 
 /* Token selection of Sec. 3.3.  PER_HEAD: every KV head keeps its own
@@ -120,6 +125,8 @@ typedef struct selkv_params {
   float gate_temperature;    /* T > 0 */
   double budget_ratio;       /* rho in (0, 1]; m = floor(rho * n) computed in IEEE double (Sec. 3.1) */
   int32_t select_mode;       /* selkv_select_mode (default PER_HEAD) */
+  int32_t merge_keys;        /* 0: keys gathered (Eq. 5 defines only values; default); 1: keys merged with
+                                the value weights of Eq. 5 (the alternative reading) */
 } selkv_params;
 
 /* Fill `p` with the paper's defaults (App. F: W = 32, K = 5, B = 32,
@@ -194,7 +201,13 @@ SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, i
  * 0 in DROP, 1 in MERGE_ALL; unrouted tokens get g = 0.
  * Merge: V~_i = (a_i v_i + sum_{j->i} g_j a_j v_j) / (a_i + sum g_j a_j);
  * a kept token that absorbs nothing is copied bit for bit.  Keys are not
- * merged: K~_i = k_i.
+ * merged (K~_i = k_i) unless merge_keys = 1, which gives them the same
+ * weights as the values.  BUCKET_NEAREST routes like BUCKET where a bucket
+ * keeps a token and sends the tokens of a bucket that keeps none to the
+ * kept token nearest by position (the lower one when equally near); a run
+ * of such buckets is absorbed by the non-empty buckets on either side, so
+ * the merge stays bucket-local (it takes the run's positions from kept_idx,
+ * whose complement evicted_idx must be).
  * In:  K, V [B, H_kv, n, d]; attn, vnorm [B, H_kv, n] (from selkv_score);
  *      kept_idx, evicted_idx (from selkv_select).  Every kept token must
  *      have attn > 0.
@@ -217,8 +230,9 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
  * the fp32 sum of (R - 1) in head order divided by H_kv.
  * In:  attn [B, H_kv, n]; kept_idx, evicted_idx; target, gate (from
  *      selkv_merge with the same params: under BUCKET routing every routed
- *      token lies in its target's bucket, which this call relies on; under
- *      FULL_COSINE any target slot is allowed).
+ *      token lies in its target's bucket, and under BUCKET_NEAREST in it
+ *      or in the run of empty buckets beside it on the nearer side, which
+ *      this call relies on; under FULL_COSINE any target slot is allowed).
  * Out: bias [B, H_kv, m] fp32.
  * Workspace: selkv_workspace_size(p, SELKV_CALL_BIAS, 0) (UNION adds the
  *      per-head ratios). */

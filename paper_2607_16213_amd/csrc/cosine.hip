@@ -466,7 +466,8 @@ struct GroupMergeArgs {
 
 // One wave per kept slot: Eq. 5 (and the Eq. 6 bias when `bias` is set) over
 // the slot's ascending list; lane group q takes list entries q, q+4, ...
-template <typename T, int D, bool VALUES>
+// MK (values mode only): keys merged with the value weights instead of gathered
+template <typename T, int D, bool VALUES, bool MK>
 __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a) {
   constexpr int E = Slice<T, D>::kElems;
   constexpr int RB = D * (int)sizeof(T);
@@ -486,9 +487,11 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
   const int l0 = oh[s], l1 = oh[s + 1];
   const float a_s = ah[pos];
 
-  float acc[E];
+  float acc[E], kacc[MK ? E : 1];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int e = 0; e < (MK ? E : 1); ++e) kacc[e] = 0.f;
   float wsum = 0.f;
   for (int lb = l0; lb < l1; lb += 64) {
     // lane-parallel metadata of up to 64 list entries
@@ -512,7 +515,7 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     for (int ib0 = 0; ib0 < cnt; ib0 += 4 * kBatch) {
       int jj[kBatch];
       float wv[kBatch];
-      RawSlice<T, D> vr[kBatch];
+      RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = ib0 + 4 * u + grp;
@@ -524,12 +527,20 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
       }
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) vr[u].load(a.V + ((size_t)head * n + jj[u]) * RB, col);
+      if constexpr (MK) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) kre[u].load(a.K + ((size_t)head * n + jj[u]) * RB, col);
+      }
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = ib0 + 4 * u + grp;
         if (i < cnt) {
 #pragma unroll
           for (int e = 0; e < E; ++e) acc[e] = fmaf(wv[u], vr[u].get(e), acc[e]);
+          if constexpr (MK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) kacc[e] = fmaf(wv[u], kre[u].get(e), kacc[e]);
+          }
           wsum += wv[u];
         }
       }
@@ -545,6 +556,13 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     acc[e] += xor_shfl(acc[e], 16);
     acc[e] += xor_shfl(acc[e], 32);
   }
+  if constexpr (MK) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      kacc[e] += xor_shfl(kacc[e], 16);
+      kacc[e] += xor_shfl(kacc[e], 32);
+    }
+  }
   wsum += xor_shfl(wsum, 16);
   wsum += xor_shfl(wsum, 32);
   if (grp == 0) {
@@ -553,14 +571,22 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     RawSlice<T, D> kr, vr;
     kr.load(krow, col);
     vr.load(vrow, col);
-    kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
     if (wsum > 0.f) {
       const float den = a_s + wsum;
       RawSlice<T, D> mv;
 #pragma unroll
       for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_s, vr.get(e), acc[e]) / den);
       mv.store(a.V_out + ((size_t)head * m + s) * RB, col);
+      if constexpr (MK) {
+        RawSlice<T, D> mk;
+#pragma unroll
+        for (int e = 0; e < E; ++e) mk.put(e, fmaf(a_s, kr.get(e), kacc[e]) / den);
+        mk.store(a.K_out + ((size_t)head * m + s) * RB, col);
+      } else {
+        kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
+      }
     } else {
+      kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
       vr.store(a.V_out + ((size_t)head * m + s) * RB, col);
     }
   }
@@ -629,7 +655,7 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
                               const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
-                              hipStream_t st) {
+                              bool merge_keys, hipStream_t st) {
   const char* w = static_cast<const char*>(ws);
   GroupMergeArgs a{};
   a.K = static_cast<const char*>(K);
@@ -649,10 +675,14 @@ hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, con
   a.raw = raw ? 1 : 0;
   const dim3 grid((s.m + kWaves - 1) / kWaves, (unsigned)s.heads);
   const bool values = bias == nullptr;
-#define SELKV_GM(T, D)                                                                        \
-  do {                                                                                        \
-    if (values) hipLaunchKernelGGL((group_merge_kernel<T, D, true>), grid, dim3(kThreads), 0, st, a); \
-    else hipLaunchKernelGGL((group_merge_kernel<T, D, false>), grid, dim3(kThreads), 0, st, a);       \
+#define SELKV_GM(T, D)                                                                                     \
+  do {                                                                                                     \
+    if (values && merge_keys)                                                                              \
+      hipLaunchKernelGGL((group_merge_kernel<T, D, true, true>), grid, dim3(kThreads), 0, st, a);          \
+    else if (values)                                                                                       \
+      hipLaunchKernelGGL((group_merge_kernel<T, D, true, false>), grid, dim3(kThreads), 0, st, a);         \
+    else                                                                                                   \
+      hipLaunchKernelGGL((group_merge_kernel<T, D, false, false>), grid, dim3(kThreads), 0, st, a);        \
   } while (0)
   if (dtype == SELKV_BF16) {
     if (s.d == 128) SELKV_GM(bf16_t, 128);

@@ -67,11 +67,12 @@ hipError_t launch_bucket_offsets(const Shape& s, int bucket, const int32_t* kept
 hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
                                const void* K, const void* V, const float* attn, const float* vnorm,
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
-                               void* V_out, int32_t* target, float* gate, hipStream_t st);
+                               void* V_out, int32_t* target, float* gate, bool merge_keys, bool nearest,
+                               hipStream_t st);
 // raw: write R - 1 = absorbed / a instead of alpha * ln R (the union mode averages it)
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
-                              const float* gate, float* bias, bool raw, hipStream_t st);
+                              const float* gate, float* bias, bool raw, bool nearest, hipStream_t st);
 hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
                                const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
                                float* gate, hipStream_t st);
@@ -79,7 +80,7 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
                               const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
-                              hipStream_t st);
+                              bool merge_keys, hipStream_t st);
 hipError_t launch_union_select(const Shape& s, const UnionPlan& p, const float* score, int32_t* kept,
                                int32_t* evicted, void* ws, hipStream_t st);
 hipError_t launch_union_bias(const Shape& s, const float* r1, float* bias, float alpha, hipStream_t st);

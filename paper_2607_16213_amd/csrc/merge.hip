@@ -11,6 +11,9 @@
 //            gather every kept key
 //   bias     per bucket: R = 1 + (sum over routed tokens of g*a) / a_i,
 //            bias = alpha * ln R (exactly 0 when nothing was absorbed)
+// Options: keys merged with the value weights (merge_keys), and the
+// nearest-kept fallback, under which the waves of the non-empty buckets also
+// absorb the runs of empty buckets beside them (still local, still ordered).
 // Row layout of one wave: lane group g = lane / 16 takes one token (row) and
 // each of its 16 lanes one contiguous slice of d/16 elements, so a wave
 // instruction moves four consecutive rows.
@@ -75,7 +78,123 @@ struct MergeArgs {
   float tau, inv_temp;
 };
 
-template <typename T, int D>
+// Nearest-kept fallback: the evicted tokens of the empty buckets between two
+// non-empty ones all lie between the last kept token P before them and the
+// first kept token Q after them, so they go to P up to floor((P + Q) / 2)
+// (the lower one when equally near) and to Q beyond.  A run before the first
+// or after the last non-empty bucket goes wholly to that bucket's outer kept
+// token.  For the non-empty bucket [bstart, bend) with kept slots [k0, k1)
+// this gives the evicted-index ranges it absorbs on either side:
+// [eL0, eL1) into slot k0 (positions e + k0) and [eR0, eR1) into slot k1 - 1
+// (positions e + k1); the ranges of neighbouring buckets meet exactly.
+struct GapRuns {
+  int eL0, eL1, eR0, eR1;
+};
+
+__device__ __forceinline__ GapRuns gap_runs(const int32_t* kh, int n, int m, int B, int bstart, int bend, int k0,
+                                            int k1) {
+  GapRuns r;
+  int jL0 = 0;
+  if (k0 > 0) {
+    const int P = kh[k0 - 1], Q = kh[k0];
+    jL0 = max((P / B + 1) * B, (int)(((int64_t)P + Q) / 2) + 1);
+  }
+  jL0 = min(max(jL0, 0), bstart);
+  int jR1 = n;
+  if (k1 < m) {
+    const int P = kh[k1 - 1], Q = kh[k1];
+    jR1 = min((Q / B) * B, (int)(((int64_t)P + Q) / 2) + 1);
+  }
+  jR1 = min(max(jR1, bend), n);
+  // clamped so that an inconsistent kept list cannot leave [0, n - m)
+  r.eL1 = bstart - k0;
+  r.eL0 = min(max(jL0 - k0, 0), r.eL1);
+  r.eR0 = bend - k1;
+  r.eR1 = max(min(jR1 - k1, n - m), r.eR0);
+  return r;
+}
+
+// Absorb the evicted entries [ea, eb) (positions e + shift, consecutive) into
+// kept slot `slot` with value vt and norm vn_t: gate each by its value cosine
+// with vt, accumulate g*a*v (and g*a*k under MK) in a fixed order, and write
+// target and gate.  Wave-uniform trip counts; lane group q takes entries 4u + q.
+template <typename T, int D, bool MK>
+__device__ __forceinline__ void absorb_run(const MergeArgs& a, const char* Kh, const char* Vh, const float* ah,
+                                           const float* vnh, int32_t* th, float* gh, int ea, int eb, int shift,
+                                           int slot, const float (&vt)[Slice<T, D>::kElems], float vn_t,
+                                           float (&acc)[Slice<T, D>::kElems],
+                                           float (&kacc)[MK ? Slice<T, D>::kElems : 1], float& wsum, int lane,
+                                           int grp, int col) {
+  constexpr int E = Slice<T, D>::kElems;
+  constexpr int RB = D * (int)sizeof(T);
+  constexpr int kBatch = 4;
+  for (int c0 = ea; c0 < eb; c0 += 64) {
+    const int cnt = min(64, eb - c0);
+    const int pos_l = c0 + shift + min(lane, cnt - 1);
+    const float a_l = ah[pos_l], vn_l = vnh[pos_l];
+    for (int ib0 = 0; ib0 < cnt; ib0 += 4 * kBatch) {
+      int jj[kBatch];
+      float ajv[kBatch], vnjv[kBatch];
+      RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        const int src = i < cnt ? i : 0;
+        jj[u] = c0 + shift + src;
+        ajv[u] = __shfl(a_l, src, 64);
+        vnjv[u] = __shfl(vn_l, src, 64);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) vr[u].load(Vh + (size_t)jj[u] * RB, col);
+      if constexpr (MK) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) kre[u].load(Kh + (size_t)jj[u] * RB, col);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
+        dot = sum16(dot);
+        float g = 0.f;
+        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
+          g = 1.f;
+        } else if (a.gate_mode == SELKV_GATE_COSINE) {
+          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
+          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
+        }
+        if (i < cnt) {
+          const float w = g * ajv[u];
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
+          if constexpr (MK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) kacc[e] = fmaf(w, kre[u].get(e), kacc[e]);
+          }
+          wsum += w;
+          if (col == 0) {
+            th[c0 + i] = slot;
+            gh[c0 + i] = g;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void reduce_groups(float (&x)[N]) {
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    x[e] += xor_shfl(x[e], 16);
+    x[e] += xor_shfl(x[e], 32);
+  }
+}
+
+// MK: keys merged with the value weights (the merge_keys reading) instead of gathered.
+// NR: nearest-kept fallback; a bucket that keeps no token is absorbed by its neighbours.
+template <typename T, int D, bool MK, bool NR>
 __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   constexpr int E = Slice<T, D>::kElems;
   constexpr int RB = D * (int)sizeof(T);
@@ -104,6 +223,7 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   const int e0 = start - k0, e1 = end - k1;
   if (k0 > k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // inconsistent kept list
   const int nk = k1 - k0, ne = e1 - e0;   // both <= B <= 64
+  if (NR && nk == 0) return;               // the neighbouring buckets absorb this one
 
   // lane-parallel metadata of the bucket: lane i holds kept entry i and evicted entry i
   int pos_k = 0, pos_e = 0;
@@ -144,9 +264,11 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
     for (int e = 0; e < E; ++e) vt[e] = 0.f;
   }
 
-  float acc[E];
+  float acc[E], kacc[MK ? E : 1];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int e = 0; e < (MK ? E : 1); ++e) kacc[e] = 0.f;
   float wsum = 0.f;
   // evicted rows, kBatch per lane group with their loads issued together;
   // lane group q takes entries 4u + q (uniform trip count, masked)
@@ -154,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   for (int ib0 = 0; ib0 < ne; ib0 += 4 * kBatch) {
     int jj[kBatch];
     float ajv[kBatch], vnjv[kBatch];
-    RawSlice<T, D> vr[kBatch];
+    RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int i = ib0 + 4 * u + grp;
@@ -165,6 +287,10 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) vr[u].load(Vh + (size_t)jj[u] * RB, col);
+    if constexpr (MK) {
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) kre[u].load(Kh + (size_t)jj[u] * RB, col);
+    }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int i = ib0 + 4 * u + grp;
@@ -186,6 +312,10 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
         const float w = g * ajv[u];
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
+        if constexpr (MK) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) kacc[e] = fmaf(w, kre[u].get(e), kacc[e]);
+        }
         wsum += w;
         if (col == 0) {
           th[e0 + i] = tslot;
@@ -194,16 +324,50 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
       }
     }
   }
-  // combine the four lane groups (fixed order)
+  // nearest-kept fallback: the runs of empty buckets on either side
+  constexpr int EN = NR ? E : 1, EK = NR && MK ? E : 1;
+  float accf[EN], kaccf[EK], accl[EN], kaccl[EK];
+  float wf = 0.f, wl = 0.f;
+  if constexpr (NR) {
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    acc[e] += xor_shfl(acc[e], 16);
-    acc[e] += xor_shfl(acc[e], 32);
+    for (int e = 0; e < E; ++e) accf[e] = accl[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EK; ++e) kaccf[e] = kaccl[e] = 0.f;
+    const GapRuns r = gap_runs(kh, n, m, a.B, start, end, k0, k1);
+    const int pf = __shfl(pos_k, 0, 64), pl = __shfl(pos_k, nk - 1, 64);
+    if (r.eL1 > r.eL0) {
+      float vf[E];
+      load_slice<T, D>(Vh + (size_t)pf * RB, col, vf);
+      absorb_run<T, D, MK>(a, Kh, Vh, ah, vnh, th, gh, r.eL0, r.eL1, k0, k0, vf, vnh[pf], accf, kaccf, wf, lane, grp,
+                           col);
+    }
+    if (r.eR1 > r.eR0) {
+      float vl[E];
+      load_slice<T, D>(Vh + (size_t)pl * RB, col, vl);
+      absorb_run<T, D, MK>(a, Kh, Vh, ah, vnh, th, gh, r.eR0, r.eR1, k1, k1 - 1, vl, vnh[pl], accl, kaccl, wl, lane,
+                           grp, col);
+    }
   }
+
+  // combine the four lane groups (fixed order)
+  reduce_groups(acc);
+  if constexpr (MK) reduce_groups(kacc);
   wsum += xor_shfl(wsum, 16);
   wsum += xor_shfl(wsum, 32);
+  if constexpr (NR) {
+    reduce_groups(accf);
+    reduce_groups(accl);
+    if constexpr (MK) {
+      reduce_groups(kaccf);
+      reduce_groups(kaccl);
+    }
+    wf += xor_shfl(wf, 16);
+    wf += xor_shfl(wf, 32);
+    wl += xor_shfl(wl, 16);
+    wl += xor_shfl(wl, 32);
+  }
 
-  // write the bucket's kept rows: keys gathered, values copied or merged;
+  // write the bucket's kept rows: keys gathered (or merged), values copied or merged;
   // kBatch rows per lane group loaded before any is stored
   for (int kb0 = 0; kb0 < nk; kb0 += 4 * kBatch) {
     RawSlice<T, D> kr[kBatch], vr[kBatch];
@@ -214,19 +378,63 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
       kr[u].load(Kh + (size_t)pos * RB, col);
       vr[u].load(Vh + (size_t)pos * RB, col);
     }
+    float akv[NR ? kBatch : 1];
+    if constexpr (NR) {
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = kb0 + 4 * u + grp;
+        akv[u] = __shfl(a_k, i < nk ? i : 0, 64);
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int i = kb0 + 4 * u + grp;
       if (i < nk) {
         const int k = k0 + i;
-        kr[u].store(Ko + (size_t)k * RB, col);
-        if (k == tslot && wsum > 0.f) {
+        if constexpr (NR) {
+          // up to three sources: the bucket's own tokens, the left run, the right run
+          const bool own = k == tslot, left = k == k0, right = k == k1 - 1;
+          const float w = (own ? wsum : 0.f) + (left ? wf : 0.f) + (right ? wl : 0.f);
+          if (w > 0.f) {
+            const float ak = akv[u], den = ak + w;
+            RawSlice<T, D> mv;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+              const float num = (own ? acc[e] : 0.f) + (left ? accf[e] : 0.f) + (right ? accl[e] : 0.f);
+              mv.put(e, fmaf(ak, vr[u].get(e), num) / den);
+            }
+            mv.store(Vo + (size_t)k * RB, col);
+            if constexpr (MK) {
+              RawSlice<T, D> mk;
+#pragma unroll
+              for (int e = 0; e < E; ++e) {
+                const float num = (own ? kacc[e] : 0.f) + (left ? kaccf[e] : 0.f) + (right ? kaccl[e] : 0.f);
+                mk.put(e, fmaf(ak, kr[u].get(e), num) / den);
+              }
+              mk.store(Ko + (size_t)k * RB, col);
+            } else {
+              kr[u].store(Ko + (size_t)k * RB, col);
+            }
+          } else {
+            kr[u].store(Ko + (size_t)k * RB, col);
+            vr[u].store(Vo + (size_t)k * RB, col);
+          }
+        } else if (k == tslot && wsum > 0.f) {
           const float den = a_t + wsum;
           RawSlice<T, D> mv;
 #pragma unroll
           for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_t, vt[e], acc[e]) / den);
           mv.store(Vo + (size_t)k * RB, col);
+          if constexpr (MK) {
+            RawSlice<T, D> mk;
+#pragma unroll
+            for (int e = 0; e < E; ++e) mk.put(e, fmaf(a_t, kr[u].get(e), kacc[e]) / den);
+            mk.store(Ko + (size_t)k * RB, col);
+          } else {
+            kr[u].store(Ko + (size_t)k * RB, col);
+          }
         } else {
+          kr[u].store(Ko + (size_t)k * RB, col);
           vr[u].store(Vo + (size_t)k * RB, col);
         }
       }
@@ -329,6 +537,70 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   }
 }
 
+// Sum of g * a over the evicted entries [ea, eb) (positions e + shift) whose
+// target is `slot`; the wave total, in a fixed order.
+__device__ __forceinline__ float run_mass(const BiasArgs& a, const int32_t* th, const float* gh, const float* ah,
+                                          int ea, int eb, int shift, int slot, int lane) {
+  float tot = 0.f;
+  for (int c0 = ea; c0 < eb; c0 += 64) {
+    const int e = c0 + lane;
+    if (e < eb && th[e] == slot) tot += gh[e] * ah[e + shift];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
+  return tot;
+}
+
+// Nearest-kept fallback: one wave per non-empty bucket adds to its kept
+// slots the bucket's own routed tokens and, for its outer slots, the runs of
+// empty buckets on either side (the split of the merge).
+__global__ __launch_bounds__(kThreads) void bias_nearest_kernel(BiasArgs a) {
+  const int64_t head = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int bucket = blockIdx.x * kWavesPerBlock + wave;
+  if (bucket >= a.nb) return;
+  const int n = a.n, m = a.m;
+  const int32_t* kh = a.kept + (size_t)head * m;
+  const int32_t* eh = a.evicted + (size_t)head * (n - m);
+  const int32_t* th = a.target + (size_t)head * (n - m);
+  const float* gh = a.gate + (size_t)head * (n - m);
+  const int32_t* oh = a.offs + (size_t)head * (a.nb + 1);
+  const float* ah = a.attn + (size_t)head * n;
+  const int start = bucket * a.B, end = min(n, start + a.B);
+  const int k0 = oh[bucket], k1 = oh[bucket + 1];
+  const int e0 = start - k0, e1 = end - k1;
+  if (k0 >= k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // empty bucket or inconsistent list
+  const int nk = k1 - k0, ne = e1 - e0;
+  const int t_e = lane < ne ? th[e0 + lane] : -1;
+  const float c_e = lane < ne ? gh[e0 + lane] * ah[eh[e0 + lane]] : 0.f;
+  const float a_k = lane < nk ? ah[kh[k0 + lane]] : 1.f;
+  const int k = k0 + lane;
+  float absorbed = 0.f;
+  // the routing sends the bucket's own tokens to one slot: one wave sum;
+  // otherwise per slot in ascending evicted order
+  const int t0 = __shfl(t_e, 0, 64);
+  if (__ballot(lane >= ne || t_e == t0) == ~0ull) {
+    float tot = c_e;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
+    absorbed = (k == t0) ? tot : 0.f;
+  } else {
+    for (int i = 0; i < ne; ++i) {
+      const int t = __shfl(t_e, i, 64);
+      const float c = __shfl(c_e, i, 64);
+      if (t == k) absorbed += c;
+    }
+  }
+  const GapRuns r = gap_runs(kh, n, m, a.B, start, end, k0, k1);
+  const float left = run_mass(a, th, gh, ah, r.eL0, r.eL1, k0, k0, lane);
+  const float right = run_mass(a, th, gh, ah, r.eR0, r.eR1, k1, k1 - 1, lane);
+  if (k == k0) absorbed += left;
+  if (k == k1 - 1) absorbed += right;
+  if (lane < nk)
+    a.bias[(size_t)head * m + k] =
+        absorbed > 0.f ? (a.raw ? absorbed / a_k : a.alpha * log1pf(absorbed / a_k)) : 0.f;
+}
+
 }  // namespace
 
 size_t bucket_offsets_bytes(const Shape& s) {
@@ -344,7 +616,8 @@ hipError_t launch_bucket_offsets(const Shape& s, int bucket, const int32_t* kept
 hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
                                const void* K, const void* V, const float* attn, const float* vnorm,
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
-                               void* V_out, int32_t* target, float* gate, hipStream_t st) {
+                               void* V_out, int32_t* target, float* gate, bool merge_keys, bool nearest,
+                               hipStream_t st) {
   MergeArgs a{};
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);
@@ -365,23 +638,30 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
   a.tau = tau;
   a.inv_temp = 1.f / temp;
   const dim3 grid((s.nb + kWavesPerBlock - 1) / kWavesPerBlock, (unsigned)s.heads);
+#define SELKV_MB(T, D)                                                                                    \
+  do {                                                                                                    \
+    if (nearest) {                                                                                        \
+      if (merge_keys) hipLaunchKernelGGL((merge_bucket_kernel<T, D, true, true>), grid, dim3(kThreads), 0, st, a); \
+      else hipLaunchKernelGGL((merge_bucket_kernel<T, D, false, true>), grid, dim3(kThreads), 0, st, a);          \
+    } else {                                                                                              \
+      if (merge_keys) hipLaunchKernelGGL((merge_bucket_kernel<T, D, true, false>), grid, dim3(kThreads), 0, st, a); \
+      else hipLaunchKernelGGL((merge_bucket_kernel<T, D, false, false>), grid, dim3(kThreads), 0, st, a);          \
+    }                                                                                                     \
+  } while (0)
   if (dtype == SELKV_BF16) {
-    if (s.d == 128)
-      hipLaunchKernelGGL((merge_bucket_kernel<bf16_t, 128>), grid, dim3(kThreads), 0, st, a);
-    else
-      hipLaunchKernelGGL((merge_bucket_kernel<bf16_t, 64>), grid, dim3(kThreads), 0, st, a);
+    if (s.d == 128) SELKV_MB(bf16_t, 128);
+    else SELKV_MB(bf16_t, 64);
   } else {
-    if (s.d == 128)
-      hipLaunchKernelGGL((merge_bucket_kernel<float, 128>), grid, dim3(kThreads), 0, st, a);
-    else
-      hipLaunchKernelGGL((merge_bucket_kernel<float, 64>), grid, dim3(kThreads), 0, st, a);
+    if (s.d == 128) SELKV_MB(float, 128);
+    else SELKV_MB(float, 64);
   }
+#undef SELKV_MB
   return hipGetLastError();
 }
 
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
-                              const float* gate, float* bias, bool raw, hipStream_t st) {
+                              const float* gate, float* bias, bool raw, bool nearest, hipStream_t st) {
   BiasArgs a{};
   a.raw = raw ? 1 : 0;
   a.attn = attn;
@@ -396,6 +676,11 @@ hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const flo
   a.nb = s.nb;
   a.B = bucket;
   a.alpha = alpha;
+  if (nearest) {
+    const dim3 grid((s.nb + kWavesPerBlock - 1) / kWavesPerBlock, (unsigned)s.heads);
+    hipLaunchKernelGGL(bias_nearest_kernel, grid, dim3(kThreads), 0, st, a);
+    return hipGetLastError();
+  }
   const int per_block = kWavesPerBlock * kBiasBuckets;
   const dim3 grid((s.nb + per_block - 1) / per_block, (unsigned)s.heads);
   hipLaunchKernelGGL(bias_bucket_kernel, grid, dim3(kThreads), 0, st, a);

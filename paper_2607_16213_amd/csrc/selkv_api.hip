@@ -29,7 +29,8 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
   if (!(p->gate_temperature > 0.f) || !isfinite(p->gate_temperature) || !isfinite(p->gate_threshold))
     return SELKV_EINVAL;
   if (p->gate_mode < SELKV_GATE_COSINE || p->gate_mode > SELKV_GATE_MERGE_ALL) return SELKV_EINVAL;
-  if (p->route_mode != SELKV_ROUTE_BUCKET && p->route_mode != SELKV_ROUTE_FULL_COSINE) return SELKV_EINVAL;
+  if (p->route_mode < SELKV_ROUTE_BUCKET || p->route_mode > SELKV_ROUTE_BUCKET_NEAREST) return SELKV_EINVAL;
+  if (p->merge_keys != 0 && p->merge_keys != 1) return SELKV_EINVAL;
   if (p->select_mode != SELKV_SELECT_PER_HEAD && p->select_mode != SELKV_SELECT_UNION) return SELKV_EINVAL;
   const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
   if (heads > 65535) return SELKV_EUNSUPPORTED;              // grid y dimension
@@ -61,12 +62,16 @@ selkv_status hip_status(hipError_t e) { return e == hipSuccess ? SELKV_OK : SELK
 
 bool is_union(const selkv_params* p) { return p->select_mode == SELKV_SELECT_UNION; }
 
-// bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
-size_t bias_base_bytes(const selkv_params* p, const Shape& s) {
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// merge and bias workspace: the bucket offsets under the bucket routings,
+// the grouping by target slot under full-cosine routing
+size_t merge_bytes(const selkv_params* p, const Shape& s) {
   return p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
 }
 
-size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+// bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
+size_t bias_base_bytes(const selkv_params* p, const Shape& s) { return merge_bytes(p, s); }
 
 selkv_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return SELKV_OK;
@@ -128,9 +133,7 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
   switch (call) {
     case SELKV_CALL_SCORE: *bytes = plan_score(s, p->kv_dtype).bytes; return SELKV_OK;
     case SELKV_CALL_SELECT: *bytes = is_union(p) ? plan_union(s).select_bytes : 0; return SELKV_OK;
-    case SELKV_CALL_MERGE:
-      *bytes = p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
-      return SELKV_OK;
+    case SELKV_CALL_MERGE: *bytes = merge_bytes(p, s); return SELKV_OK;
     case SELKV_CALL_BIAS:
       *bytes = bias_base_bytes(p, s);
       if (is_union(p)) *bytes = round256(*bytes) + plan_union(s).ratio_bytes;
@@ -184,25 +187,28 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
       !aligned(vnorm, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
       !aligned(gate, 4))
     return SELKV_EALIGN;
-  if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {
-    const GroupPlan gp = plan_group(s);
-    if ((st = check_ws(ws, ws_bytes, gp.bytes)) != SELKV_OK) return st;
-    hipError_t e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm,
-                                       kept_idx, evicted_idx, target, gate, stream);
+  if ((st = check_ws(ws, ws_bytes, merge_bytes(p, s))) != SELKV_OK) return st;
+  const bool mk = p->merge_keys != 0;
+  hipError_t e;
+  if (p->route_mode != SELKV_ROUTE_FULL_COSINE) {
+    // bucket routings: one wave per bucket (plus its runs of empty buckets under the nearest-kept fallback)
+    int32_t* offs = static_cast<int32_t*>(ws);
+    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
     if (e != hipSuccess) return SELKV_EHIP;
-    e = launch_group(s, gp, target, ws, stream);
-    if (e != hipSuccess) return SELKV_EHIP;
-    return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out,
-                                         V_out, nullptr, 0.f, false, stream));
+    return hip_status(launch_merge_bucket(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
+                                          p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs, K_out,
+                                          V_out, target, gate, mk, p->route_mode == SELKV_ROUTE_BUCKET_NEAREST,
+                                          stream));
   }
-  const size_t need = bucket_offsets_bytes(s);
-  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
-  int32_t* offs = static_cast<int32_t*>(ws);
-  hipError_t e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+  // all-pairs routing: match, group by target slot, merge per slot
+  e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm, kept_idx,
+                          evicted_idx, target, gate, stream);
   if (e != hipSuccess) return SELKV_EHIP;
-  e = launch_merge_bucket(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold, p->gate_temperature, K, V,
-                          attn, vnorm, kept_idx, evicted_idx, offs, K_out, V_out, target, gate, stream);
-  return hip_status(e);
+  const GroupPlan gp = plan_group(s);
+  e = launch_group(s, gp, target, ws, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out, V_out,
+                                       nullptr, 0.f, false, mk, stream));
 }
 
 SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,
@@ -230,12 +236,13 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
     e = launch_group(s, gp, target, ws, stream);
     if (e != hipSuccess) return SELKV_EHIP;
     e = launch_group_merge(s, gp, p->kv_dtype, nullptr, nullptr, attn, kept_idx, evicted_idx, gate, ws, nullptr,
-                           nullptr, dst, p->alpha, uni, stream);
+                           nullptr, dst, p->alpha, uni, false, stream);
   } else {
     int32_t* offs = static_cast<int32_t*>(ws);
     e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
     if (e != hipSuccess) return SELKV_EHIP;
-    e = launch_bias_bucket(s, p->bucket, p->alpha, attn, kept_idx, evicted_idx, offs, target, gate, dst, uni, stream);
+    e = launch_bias_bucket(s, p->bucket, p->alpha, attn, kept_idx, evicted_idx, offs, target, gate, dst, uni,
+                           p->route_mode == SELKV_ROUTE_BUCKET_NEAREST, stream);
   }
   if (e != hipSuccess || !uni) return hip_status(e);
   return hip_status(launch_union_bias(s, dst, bias, p->alpha, stream));

@@ -18,14 +18,14 @@ LIB_PATH = os.path.join(_PKG, "libselkv.so")
 
 F32, BF16 = 0, 1
 GATE_COSINE, GATE_DROP, GATE_MERGE_ALL = 0, 1, 2
-ROUTE_BUCKET, ROUTE_FULL_COSINE = 0, 1
+ROUTE_BUCKET, ROUTE_FULL_COSINE, ROUTE_BUCKET_NEAREST = 0, 1, 2
 SELECT_PER_HEAD, SELECT_UNION = 0, 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE = range(5)
 STATUS = {0: "SELKV_OK", 1: "SELKV_EINVAL", 2: "SELKV_EDTYPE", 3: "SELKV_EUNSUPPORTED", 4: "SELKV_EALIGN",
           5: "SELKV_EWORKSPACE", 6: "SELKV_EHIP"}
 GATE_MODES = {"cosine": GATE_COSINE, "drop": GATE_DROP, "merge_all": GATE_MERGE_ALL}
-ROUTE_MODES = {"bucket": ROUTE_BUCKET, "full_cosine": ROUTE_FULL_COSINE}
+ROUTE_MODES = {"bucket": ROUTE_BUCKET, "full_cosine": ROUTE_FULL_COSINE, "bucket_nearest": ROUTE_BUCKET_NEAREST}
 SELECT_MODES = {"per_head": SELECT_PER_HEAD, "union": SELECT_UNION}
 
 
@@ -56,6 +56,7 @@ class Params(ctypes.Structure):
         ("gate_temperature", ctypes.c_float),
         ("budget_ratio", ctypes.c_double),
         ("select_mode", ctypes.c_int32),
+        ("merge_keys", ctypes.c_int32),
     ]
 
 

@@ -63,7 +63,7 @@ def test_params_init_defaults(S):
     assert p.struct_size == ctypes.sizeof(S.Params)
     assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
     assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
-    assert S.lib.selkv_abi_version() == 2
+    assert S.lib.selkv_abi_version() == 3
     assert S.lib.selkv_status_string(0) == b"success"
 
 
@@ -159,3 +159,20 @@ def test_decode_append_validation(S):
     assert f(ctypes.byref(p), fake, ctypes.c_void_p(0x10008), fake, fake, fake, fake, 3, 8, fake, fake, 1 << 30,
              None) == 4
     assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 3, 8, fake, fake, 0, None) == 5
+
+
+def test_alternative_readings_validation_and_workspace(S):
+    """Nearest-kept fallback and key merging: the flags are checked, and both
+    stay bucket-local (the workspace of the plain bucket routing)."""
+    b = ctypes.c_size_t()
+    for bad in (S.params(seq_len=256, route_mode=3), S.params(seq_len=256, route_mode=-1),
+                S.params(seq_len=256, merge_keys=2)):
+        assert S.lib.selkv_workspace_size(ctypes.byref(bad), S.CALL_MERGE, 0, ctypes.byref(b)) == 1
+    plain = S.params(seq_len=256)
+    near = S.params(seq_len=256, route_mode="bucket_nearest")
+    full = S.params(seq_len=256, route_mode="full_cosine")
+    for call in (S.CALL_MERGE, S.CALL_BIAS):
+        assert S.workspace_bytes(near, call) == S.workspace_bytes(plain, call)
+        assert S.workspace_bytes(full, call) > S.workspace_bytes(plain, call)
+    keys = S.params(seq_len=256, merge_keys=1)
+    assert S.workspace_bytes(keys, S.CALL_MERGE) == S.workspace_bytes(plain, S.CALL_MERGE)

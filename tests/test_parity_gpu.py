@@ -735,3 +735,120 @@ def test_decode_with_appended_tokens(S, name):
         for (b, h) in heads:
             assert_close_rows(got[b, h * G:(h + 1) * G], ref[b, h * G:(h + 1) * G], tol, f"append step {step}")
     assert torch.equal(bias.cpu(), bh)
+
+
+# ------------------------------------------------------------------ alternative readings as modes
+READINGS = [
+    # many empty buckets: bucket 4 at a 10% budget leaves most buckets without a kept token
+    dict(batch=1, H=2, G=2, d=64, n=600, W=16, dtype="fp32", route_mode="bucket_nearest", bucket=4,
+         budget_ratio=0.1),
+    dict(batch=2, H=1, G=4, d=128, n=1000, W=32, dtype="bf16", route_mode="bucket_nearest", bucket=4,
+         budget_ratio=0.1),
+    dict(batch=1, H=2, G=2, d=128, n=777, W=16, dtype="fp32", route_mode="bucket_nearest", bucket=8,
+         budget_ratio=0.05, gate_mode=2, merge_keys=1),
+    dict(batch=1, H=1, G=2, d=64, n=300, W=8, dtype="bf16", route_mode="bucket_nearest", bucket=2,
+         budget_ratio=0.02, gate_mode=1),
+    dict(batch=1, H=1, G=2, d=64, n=200, W=8, dtype="fp32", route_mode="bucket_nearest", budget_ratio=1.0),
+    dict(batch=1, H=2, G=2, d=64, n=513, W=16, dtype="fp32", merge_keys=1),                # bucket routing
+    dict(batch=1, H=2, G=4, d=128, n=1000, W=32, dtype="bf16", merge_keys=1, gate_mode=2),
+    dict(batch=1, H=2, G=2, d=128, n=640, W=16, dtype="bf16", route_mode="bucket_nearest", bucket=4,
+         budget_ratio=0.1, merge_keys=1),
+]
+
+
+@pytest.mark.parametrize("case", READINGS, ids=[f"reading{i}" for i in range(len(READINGS))])
+def test_alternative_readings_stagewise(S, case):
+    """Nearest-kept fallback for empty buckets and key merging, each fed the
+    oracle's fp32 attention, norms and kept / evicted lists: targets are
+    integers decided on identical fp32 inputs (bit-exact), gates, merged
+    values and merged keys within the storage tolerance, gathered keys
+    bit-exact where keys are not merged, and the bias through the grouping by
+    target slot fed the oracle's targets and gates."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 11 + 3, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=6, device=DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case, **kw)
+    nearest = p.route_mode == S.ROUTE_BUCKET_NEAREST
+    mk = bool(p.merge_keys)
+    tol = TOL[case["dtype"]]
+    B, H, n, d = K.shape
+    m, mr, ms = S.budget(p)
+    comp = S.Compressor(p, DEV)
+    S.score(p, K, V, Q, comp.score, comp.attn, comp.vnorm, comp.ws_score)
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(K), np64(V), np64(Q)
+    refs = {}
+    a_in, vn_in = comp.attn.clone(), comp.vnorm.clone()
+    tau, temp = float(np.float32(p.gate_threshold)), float(np.float32(p.gate_temperature))
+    fallbacks = 0
+    for b in range(B):
+        for h in range(H):
+            ch = oracle_chain(K64[b, h], V64[b, h], Q64[b, h * p.group:(h + 1) * p.group], p, GATE[p.gate_mode])
+            comp.kept[b, h] = torch.as_tensor(ch["kept"], dtype=torch.int32)
+            comp.evicted[b, h] = torch.as_tensor(ch["ev"], dtype=torch.int32)
+            a_in[b, h] = torch.as_tensor(ch["a32"], dtype=torch.float32)
+            vn_in[b, h] = torch.as_tensor(ch["vn"], dtype=torch.float32)
+            if nearest:
+                target = O.route_bucket_nearest(ch["a32"], ch["kept"], ch["ev"], p.bucket)
+                fallbacks += int((ch["target"] < 0).sum())
+            else:
+                target = ch["target"]
+            g = O.gate(V64[b, h], ch["kept"], ch["ev"], target, GATE[p.gate_mode], tau, temp)
+            k_out, v_out, _ = O.merge(K64[b, h], V64[b, h], ch["a32"], ch["kept"], ch["ev"], target, g,
+                                      merge_keys=mk)
+            g32 = g.astype(np.float32).astype(np.float64)
+            bias = O.ratio_bias(ch["a32"], ch["kept"], ch["ev"], target, g32, float(np.float32(p.alpha)))
+            refs[(b, h)] = dict(kept=ch["kept"], target=target, g=g, g32=g32, k_out=k_out, v_out=v_out, bias=bias)
+    if nearest and n > m:
+        assert fallbacks > 0, "the case must leave some bucket without a kept token"
+    S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
+            comp.ws_merge)
+    torch.cuda.synchronize()
+    for (b, h), r in refs.items():
+        np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), r["target"], err_msg=f"target[{b},{h}]")
+        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert_close_rows(np64(comp.V_out[b, h]), r["v_out"], tol, f"V_out[{b},{h}]")
+        if mk:
+            assert_close_rows(np64(comp.K_out[b, h]), r["k_out"], tol, f"K_out[{b},{h}]")
+            untouched = np.setdiff1d(np.arange(m), r["target"][r["target"] >= 0])    # nothing routed there
+            got = comp.K_out[b, h].cpu()[torch.as_tensor(untouched, dtype=torch.long)]
+            assert torch.equal(got, K[b, h].cpu()[torch.as_tensor(r["kept"][untouched])]), "unmerged keys gathered"
+        else:
+            assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(r["kept"])]), f"K_out[{b},{h}]"
+        comp.target[b, h] = torch.as_tensor(r["target"], dtype=torch.int32)
+        comp.gate[b, h] = torch.as_tensor(r["g32"], dtype=torch.float32)
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    torch.cuda.synchronize()
+    for (b, h), r in refs.items():
+        err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
+        assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
+    print(f"nearest-kept fallbacks: {fallbacks}")
+
+
+def test_nearest_fallback_end_to_end_llama_layer(S):
+    """The whole pipeline with the nearest-kept fallback on one Llama-shaped
+    layer (bucket 8 at a 10% budget): every evicted token gets a kept target
+    (no -1), buckets that keep a token route exactly as the plain bucket
+    routing on the same call's outputs, and the run is bitwise repeatable."""
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096, n_heads_kv=4)
+    t = synth.make_layer(w, 0, DEV)
+    p_near = make_params(S, case_from_workload(w), route_mode="bucket_nearest", bucket=8, budget_ratio=0.1)
+    p_plain = make_params(S, case_from_workload(w), bucket=8, budget_ratio=0.1)
+    outs = []
+    for p in (p_near, p_near, p_plain):
+        c = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+        torch.cuda.synchronize()
+        outs.append({k: v.clone() for k, v in c.outputs().items()})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    near, plain = outs[0], outs[2]
+    assert torch.equal(near["kept"], plain["kept"])
+    tn, tp = near["target"].cpu().numpy(), plain["target"].cpu().numpy()
+    m = near["kept"].shape[2]
+    assert ((tn >= 0) & (tn < m)).all()
+    routed = tp >= 0
+    assert (~routed).any(), "a 10% budget with bucket 8 must leave empty buckets"
+    np.testing.assert_array_equal(tn[routed], tp[routed])
