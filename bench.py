@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--full-cosine-layers", type=int, default=1,
                     help="layers timed with the all-pairs cosine routing variant (0 = skip)")
     ap.add_argument("--no-generation", action="store_true", help="skip the growing-cache generation loop timing")
+    ap.add_argument("--no-rope", action="store_true", help="skip the RoPE repositioning timing")
     ap.add_argument("--no-union", action="store_true",
                     help="skip the timings of the alternative modes (GQA union, nearest-kept fallback, merged keys)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -494,7 +495,8 @@ def main():
     if not args.no_union:
         out["gqa_union"] = measure_union(job)
         out["alt_readings"] = measure_readings(job)
-    out["rope_reposition"] = measure_rope(job)
+    if not args.no_rope:
+        out["rope_reposition"] = measure_rope(job)
 
     traffic = read_traffic()
     out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),
