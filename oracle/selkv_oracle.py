@@ -44,7 +44,9 @@ Readings taken where the paper is silent or garbled:
   * alternative readings, as modes: route_bucket_nearest sends the evicted
     tokens of a bucket that keeps nothing to the nearest kept position
     instead of dropping them; merge(..., merge_keys=True) averages keys with
-    the value weights of Eq. 5.
+    the value weights of Eq. 5; route_coattention reads Eq. 3's A_{h,j,i} as
+    the co-attention sum_r A[r, j] A[r, i] over the window rows of the G
+    query heads (a sum, not a mean: the argmax does not depend on it).
 """
 from __future__ import annotations
 
@@ -244,6 +246,37 @@ def route_bucket_nearest(a: np.ndarray, kept: np.ndarray, evicted: np.ndarray, b
             continue
         dist = np.abs(kept.astype(np.int64) - int(j))
         target[e] = int(np.flatnonzero(dist == dist.min())[0])     # kept is ascending: lowest position
+    return target
+
+
+def window_attention_group(q_win_group: np.ndarray, k: np.ndarray, scale: float) -> np.ndarray:
+    """The window attention of the G query heads of one KV head stacked
+    row-wise: A [G*W, n], row h*W + i = query head h at window row i."""
+    return np.concatenate([window_attention(q_win_group[g], k, scale) for g in range(q_win_group.shape[0])])
+
+
+def route_coattention(A: np.ndarray, kept: np.ndarray, evicted: np.ndarray, bucket: int) -> np.ndarray:
+    """Alternative reading of Eq. 3 (its A_{h,j,i} taken as how much the
+    window attends to j and i together): the co-attention of evicted j and
+    kept i is sum over window rows r of A[r, j] * A[r, i], over the rows of
+    all G query heads of the KV head (A from window_attention_group).  Each
+    evicted token goes to the kept token of its own bucket with the largest
+    co-attention, lowest position on ties; a bucket with no kept token
+    routes nowhere (-1), as in Eq. 3.
+
+    Returns target [n-m]: kept slots or -1.
+    """
+    A = np.asarray(A, dtype=np.float64)
+    slots = {}
+    for slot, i in enumerate(kept):
+        slots.setdefault(int(i) // bucket, []).append(slot)
+    target = np.full(evicted.shape[0], -1, dtype=np.int64)
+    for e, j in enumerate(evicted):
+        cand = slots.get(int(j) // bucket)
+        if not cand:
+            continue
+        co = A[:, kept[cand]].T @ A[:, int(j)]
+        target[e] = cand[int(np.argmax(co))]        # first maximum: candidates ascend, lowest position
     return target
 
 
@@ -463,6 +496,10 @@ def compress_head(k, v, q_win_group, *, window=None, pool_kernel=5, recent=16, b
         target = route_bucket(a, kept, evicted, bucket)
     elif route_mode == "full_cosine":
         target, _ = route_full_cosine(v, kept, evicted)
+    elif route_mode == "bucket_nearest":
+        target = route_bucket_nearest(a, kept, evicted, bucket)
+    elif route_mode == "coattn":
+        target = route_coattention(window_attention_group(q_win_group, k, scale), kept, evicted, bucket)
     else:
         raise ValueError(route_mode)
     g = gate(v, kept, evicted, target, gate_mode, gate_threshold, gate_temperature)  # step 4

@@ -528,3 +528,73 @@ def test_merge_keys_closed_form():
     # nothing absorbed: keys stay the kept keys either way
     k_none, _, _ = O.merge(k, v, a, kept, ev, np.array([-1]), g, merge_keys=True)
     assert np.array_equal(k_none[0], k[0])
+
+
+def test_coattention_routing_hand_worked():
+    c = GOLD["coattention_routing"]
+    A, kept, ev = np.array(c["A"]), np.array(c["kept"]), np.array(c["evicted"])
+    assert O.route_bucket(A.sum(axis=0), kept, ev, c["bucket"]).tolist() == c["target_bucket"]
+    assert O.route_coattention(A, kept, ev, c["bucket"]).tolist() == c["target_coattn"]
+
+
+def test_coattention_routing_reduces_to_eq3_with_one_window_row():
+    """With one window row (G = W = 1) the co-attention of j and i is
+    A[j] * A[i] with A[j] > 0, so its argmax over the bucket is the argmax of
+    a = A: exactly the routing of Eq. 3."""
+    rng = np.random.default_rng(5)
+    for trial in range(20):
+        n, d, B = int(rng.integers(8, 120)), 16, int(rng.integers(1, 9))
+        k, q = rng.standard_normal((n, d)), rng.standard_normal((1, 1, d))
+        m = int(rng.integers(1, n))
+        kept = np.sort(rng.choice(n, m, replace=False))
+        ev = np.setdiff1d(np.arange(n), kept)
+        A = O.window_attention_group(q, k, 1.0 / 4)
+        a = O.cumulative_attention(q, k, 1.0 / 4)
+        assert np.array_equal(O.route_coattention(A, kept, ev, B), O.route_bucket(a, kept, ev, B))
+
+
+def test_coattention_routing_properties():
+    """Empty buckets route nowhere, identical candidate columns tie to the
+    lower slot, and the routing ignores the order and a common scale of the
+    window rows."""
+    rng = np.random.default_rng(9)
+    n, B = 40, 8
+    A = rng.random((6, n))
+    A /= A.sum(axis=1, keepdims=True)
+    kept = np.array([1, 3, 17, 20, 21, 39])
+    ev = np.setdiff1d(np.arange(n), kept)
+    t = O.route_coattention(A, kept, ev, B)
+    empty = (ev // B == 1) | (ev // B == 3)          # buckets 8..15 and 24..31 keep nothing
+    assert (t[empty] == -1).all() and (t[~empty] >= 0).all()
+    for e, j in enumerate(ev):
+        if t[e] >= 0:
+            assert kept[t[e]] // B == j // B
+    assert np.array_equal(O.route_coattention(A[::-1] * 3.0, kept, ev, B), t)
+    A2 = A.copy()
+    A2[:, 3] = A2[:, 1]                               # kept positions 1 and 3 get identical columns
+    t2 = O.route_coattention(A2, kept, ev, B)
+    assert (t2[ev < 8] == 0).all()
+
+
+def test_window_attention_group_equals_library_attention_per_head():
+    """The stacked window attention of G query heads: G causal SDPA calls
+    (V = identity) give head h's matrix, whose last W rows are rows
+    h*W .. h*W + W - 1 of the stack."""
+    r = rng(21)
+    n, d, W, G = 29, 8, 5, 3
+    Q = r.standard_normal((G, n, d))
+    K = r.standard_normal((n, d))
+    ref = sdpa64(Q, np.repeat(K[None], G, 0), np.repeat(np.eye(n)[None], G, 0), causal=True)[:, n - W:]
+    got = O.window_attention_group(Q[:, n - W:], K, 1.0 / math.sqrt(d))
+    assert got.shape == (G * W, n)
+    np.testing.assert_allclose(got, ref.reshape(G * W, n), rtol=1e-13, atol=1e-15)
+
+
+def test_coattention_is_linear_in_the_evicted_column():
+    """Hand case: the co-attention weighs the window rows by A[r, j] itself
+    (not its square).  A_j = (.4, .2), kept i1 = (.1, .35), i2 = (.2, .1):
+    .04 + .07 = .11 beats .08 + .02 = .10, so i1; with squared weights
+    (.16, .04) it would be .030 against .036, i2."""
+    A = np.array([[0.4, 0.1, 0.2, 0.3], [0.2, 0.35, 0.1, 0.35]])
+    t = O.route_coattention(A, np.array([1, 2]), np.array([0, 3]), 4)
+    assert t[0] == 0
