@@ -54,12 +54,13 @@ def parse():
     return ap.parse_args()
 
 
-DECODE_SOURCES = [os.path.join(ROOT, "paper_2607_16213_amd", "csrc", f)
-                  for f in ("decode.hip", "common.hpp", "internal.hpp")]
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2607_16213_amd", "csrc", f) for f in ("decode.hip", "common.hpp")]
 
 
 def source_hash(paths=DECODE_SOURCES):
-    """Hash of the sources the decode kernels are built from."""
+    """Hash of the device sources the decode kernels are built from (the
+    kernels' file and the device helpers it includes; the host-side launcher
+    declarations are left out)."""
     h = hashlib.sha256()
     for p in paths:
         h.update(open(p, "rb").read())
@@ -269,25 +270,36 @@ def measure_variant(job, note, reps=3, **modes):
     ws_sel = selkv.workspace(p, selkv.CALL_SELECT, dev)
     ws_merge = selkv.workspace(p, selkv.CALL_MERGE, dev)
     ws_bias = selkv.workspace(p, selkv.CALL_BIAS, dev)
+    coattn = p.route_mode == selkv.ROUTE_COATTN
+    ws_route = selkv.workspace(p, selkv.CALL_ROUTE, dev) if coattn else None
+    names = ("score", "select") + (("route",) if coattn else ()) + ("merge", "bias")
 
     def run(ev=None):
-        if ev: ev[0].record()
+        i = 0
+        if ev: ev[i].record()
         selkv.score(p, job.Kf, job.Vf, job.Qf, c.score, c.attn, c.vnorm, c.ws_score)
-        if ev: ev[1].record()
+        i += 1
+        if ev: ev[i].record()
         selkv.select(p, c.score, c.kept, c.evicted, ws_sel)
-        if ev: ev[2].record()
+        i += 1
+        if ev: ev[i].record()
+        if coattn:
+            selkv.route_coattn(p, job.Kf, job.Qf, c.kept, c.evicted, c.target, ws_route)
+            i += 1
+            if ev: ev[i].record()
         selkv.merge(p, job.Kf, job.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
                     ws_merge)
-        if ev: ev[3].record()
+        i += 1
+        if ev: ev[i].record()
         selkv.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, ws_bias)
-        if ev: ev[4].record()
+        i += 1
+        if ev: ev[i].record()
 
     run()
     torch.cuda.synchronize()
-    names = ("score", "select", "merge", "bias")
     tot = {k: 0.0 for k in names}
     for _ in range(reps):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
         run(ev)
         torch.cuda.synchronize()
         for i, k in enumerate(names):
@@ -307,11 +319,15 @@ def measure_union(job):
 
 def measure_readings(job):
     """The alternative readings offered as modes: the nearest-kept fallback
-    for buckets that keep no token, and keys merged with the value weights."""
+    for buckets that keep no token, keys merged with the value weights, and
+    co-attention routing."""
     return {"bucket_nearest": measure_variant(job, "route_mode bucket_nearest: empty buckets route to the nearest "
                                                    "kept token, absorbed by the neighbouring buckets' waves",
                                               route_mode="bucket_nearest"),
-            "merge_keys": measure_variant(job, "merge_keys 1: keys merged with the Eq. 5 weights", merge_keys=1)}
+            "merge_keys": measure_variant(job, "merge_keys 1: keys merged with the Eq. 5 weights", merge_keys=1),
+            "coattn": measure_variant(job, "route_mode coattn: Eq. 3 ranked by the co-attention sum_r A[r,j] A[r,i] "
+                                           "(row statistics recomputed, bucket Gram matrices on MFMA)",
+                                      route_mode="coattn")}
 
 
 def measure_generation(job, steps=64, reps=3):

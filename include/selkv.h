@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define SELKV_ABI_VERSION 3
+#define SELKV_ABI_VERSION 4
 
 typedef enum selkv_status {
   SELKV_OK = 0,
@@ -76,11 +76,14 @@ typedef enum selkv_gate_mode {
  * FULL_COSINE is the all-pairs cosine routing that Eq. 3 replaces;
  * BUCKET_NEAREST is Eq. 3 with the other reading of the empty-bucket case
  * the paper leaves open: those tokens go to the kept token nearest by
- * position (the lower position when two are equally near). */
+ * position (the lower position when two are equally near).
+ * COATTN reads Eq. 3's A_{h,j,i} as co-attention: targets come from
+ * selkv_route_coattn, and selkv_merge takes them as input. */
 typedef enum selkv_route_mode {
   SELKV_ROUTE_BUCKET = 0,
   SELKV_ROUTE_FULL_COSINE = 1,
-  SELKV_ROUTE_BUCKET_NEAREST = 2
+  SELKV_ROUTE_BUCKET_NEAREST = 2,
+  SELKV_ROUTE_COATTN = 3
 } selkv_route_mode;
 
 /* Token selection of Sec. 3.3.  PER_HEAD: every KV head keeps its own
@@ -100,7 +103,8 @@ typedef enum selkv_call {
   SELKV_CALL_SELECT = 1,
   SELKV_CALL_MERGE = 2,
   SELKV_CALL_BIAS = 3,
-  SELKV_CALL_DECODE = 4
+  SELKV_CALL_DECODE = 4,
+  SELKV_CALL_ROUTE = 5      /* selkv_route_coattn */
 } selkv_call;
 
 /* Problem description, named as in the paper.  Fill it with
@@ -187,6 +191,28 @@ SELKV_API selkv_status selkv_score(const selkv_params* p, const void* K, const v
 SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, int32_t* kept_idx,
                                     int32_t* evicted_idx, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Step 3 of Algorithm 1 under the co-attention reading of Eq. 3 (Sec. 3.4;
+ * the route_mode COATTN alternative).
+ *
+ * Eq. 3 ranks candidate targets by A_{h,j,i}, which the window pass does not
+ * produce as such; this call reads it as how much the observation window
+ * attends to evicted j and kept i together:
+ *   co(j, i) = sum over the G*W window rows r of the KV head of P[r, j] P[r, i]
+ * with P the softmax window attention of selkv_score (scale, causal mask).
+ * Evicted token j goes to the kept token of its bucket floor(j/B) with the
+ * largest co(j, i), lowest position on ties, or nowhere (-1) if the bucket
+ * keeps no token.  The row statistics over all n keys are recomputed here,
+ * then the logits of each bucket's keys and their Gram matrix P^T P are
+ * formed on MFMA; the attention matrix is never stored.
+ * In:  K [B, H_kv, n, d], Qwin [B, H_kv*G, W, d] (kv_dtype, as for
+ *      selkv_score); kept_idx, evicted_idx (from selkv_select).
+ * Out: target [B, H_kv, n - m] int32 kept slot or -1; pass it to selkv_merge
+ *      and selkv_bias with route_mode COATTN.
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_ROUTE, 0). */
+SELKV_API selkv_status selkv_route_coattn(const selkv_params* p, const void* K, const void* Qwin,
+                                          const int32_t* kept_idx, const int32_t* evicted_idx, int32_t* target,
+                                          void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Steps 3-5 of Algorithm 1: routing (Sec. 3.4, Eq. 3), soft cosine gate
  * (Sec. 3.5, Eq. 4) and gated merge (Eq. 5).
  *
@@ -207,12 +233,16 @@ SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, i
  * kept token nearest by position (the lower one when equally near); a run
  * of such buckets is absorbed by the non-empty buckets on either side, so
  * the merge stays bucket-local (it takes the run's positions from kept_idx,
- * whose complement evicted_idx must be).
+ * whose complement evicted_idx must be).  COATTN takes `target` as INPUT
+ * (from selkv_route_coattn) instead of routing: a target outside the
+ * token's own bucket counts as -1; the merge per kept slot runs over its
+ * tokens in ascending order.
  * In:  K, V [B, H_kv, n, d]; attn, vnorm [B, H_kv, n] (from selkv_score);
  *      kept_idx, evicted_idx (from selkv_select).  Every kept token must
  *      have attn > 0.
  * Out: K_out, V_out [B, H_kv, m, d] (kv_dtype; row s is kept_idx[s]);
- *      target [B, H_kv, n - m] int32 kept slot or -1; gate [B, H_kv, n - m] fp32.
+ *      target [B, H_kv, n - m] int32 kept slot or -1 (read, not written,
+ *      under COATTN); gate [B, H_kv, n - m] fp32.
  * Workspace: selkv_workspace_size(p, SELKV_CALL_MERGE, 0). */
 SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const void* V, const float* attn,
                                    const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx,
@@ -232,7 +262,8 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
  *      selkv_merge with the same params: under BUCKET routing every routed
  *      token lies in its target's bucket, and under BUCKET_NEAREST in it
  *      or in the run of empty buckets beside it on the nearer side, which
- *      this call relies on; under FULL_COSINE any target slot is allowed).
+ *      this call relies on; under COATTN a target outside the token's
+ *      bucket counts as -1; under FULL_COSINE any target slot is allowed).
  * Out: bias [B, H_kv, m] fp32.
  * Workspace: selkv_workspace_size(p, SELKV_CALL_BIAS, 0) (UNION adds the
  *      per-head ratios). */

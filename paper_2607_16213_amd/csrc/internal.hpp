@@ -69,6 +69,18 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
                                void* V_out, int32_t* target, float* gate, bool merge_keys, bool nearest,
                                hipStream_t st);
+// targets given (co-attention routing): per bucket, grouped by target slot
+hipError_t launch_merge_targets(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
+                                const void* K, const void* V, const float* attn, const float* vnorm,
+                                const int32_t* kept, const int32_t* evicted, const int32_t* offs,
+                                const int32_t* target, void* K_out, void* V_out, float* gate, bool merge_keys,
+                                hipStream_t st);
+// score pass 1 and its combine only: the row statistics at plan.stats_off of ws
+hipError_t launch_row_stats(const Shape& s, const ScorePlan& p, int dtype, float scale, const void* K,
+                            const void* Qwin, void* ws, hipStream_t st);
+hipError_t launch_coattn_route(const Shape& s, const ScorePlan& sp, int dtype, int bucket, int W, const void* K,
+                               const void* Qwin, const void* score_ws, const int32_t* kept, const int32_t* offs,
+                               int32_t* target, float c2, hipStream_t st);
 // raw: write R - 1 = absorbed / a instead of alpha * ln R (the union mode averages it)
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,

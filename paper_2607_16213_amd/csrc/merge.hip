@@ -442,6 +442,188 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   }
 }
 
+// Targets given (the co-attention routing): any kept slot of a bucket may
+// absorb any of its evicted tokens.  One wave per bucket ranks the bucket's
+// routed entries by (target, position), then merges one target slot at a
+// time over its entries in ascending position, and copies the kept rows
+// that absorbed nothing.  A target outside the token's bucket counts as -1.
+template <typename T, int D, bool MK>
+__global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
+  constexpr int E = Slice<T, D>::kElems;
+  constexpr int RB = D * (int)sizeof(T);
+  constexpr int kBatch = 4;
+  const int64_t head = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int bucket = blockIdx.x * kWavesPerBlock + wave;
+  if (bucket >= a.nb) return;   // whole wave; no block barrier below
+
+  const int n = a.n, m = a.m;
+  const int32_t* kh = a.kept + (size_t)head * m;
+  const int32_t* eh = a.evicted + (size_t)head * (n - m);
+  const int32_t* oh = a.offs + (size_t)head * (a.nb + 1);
+  const float* ah = a.attn + (size_t)head * n;
+  const float* vnh = a.vnorm + (size_t)head * n;
+  const char* Kh = a.K + (size_t)head * n * RB;
+  const char* Vh = a.V + (size_t)head * n * RB;
+  char* Ko = a.K_out + (size_t)head * m * RB;
+  char* Vo = a.V_out + (size_t)head * m * RB;
+  const int32_t* th = a.target + (size_t)head * (n - m);
+  float* gh = a.gate + (size_t)head * (n - m);
+
+  const int start = bucket * a.B;
+  const int end = min(n, start + a.B);
+  const int k0 = oh[bucket], k1 = oh[bucket + 1];
+  const int e0 = start - k0, e1 = end - k1;
+  if (k0 > k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // inconsistent kept list
+  const int nk = k1 - k0, ne = e1 - e0;   // both <= B <= 64
+
+  int pos_k = 0, pos_e = 0, t_e = -1;
+  float a_k = 1.f, a_e = 0.f, vn_e = 0.f;
+  if (lane < nk) {
+    pos_k = kh[k0 + lane];
+    a_k = ah[pos_k];
+  }
+  if (lane < ne) {
+    pos_e = eh[e0 + lane];
+    a_e = ah[pos_e];
+    vn_e = vnh[pos_e];
+    const int t = th[e0 + lane];
+    t_e = (t >= k0 && t < k1) ? t : -1;
+    if (t_e < 0) gh[e0 + lane] = 0.f;
+  }
+  const bool routed = t_e >= 0;
+  // rank by (target, lane); unrouted lanes after every routed one
+  const int key = routed ? t_e : 0x7fffffff;
+  int rank = 0;
+  for (int q = 0; q < 64; ++q) {
+    const int kq = __builtin_amdgcn_readlane(key, q);
+    rank += (kq < key || (kq == key && q < lane)) ? 1 : 0;
+  }
+  int src = 0;   // the lane whose rank is this lane
+  for (int q = 0; q < 64; ++q)
+    if (__builtin_amdgcn_readlane(rank, q) == lane) src = q;
+  const int nrouted = __popcll(__ballot(routed));
+  const int s_t = __shfl(t_e, src, 64), s_pos = __shfl(pos_e, src, 64);
+  const float s_a = __shfl(a_e, src, 64), s_vn = __shfl(vn_e, src, 64);
+  const int prev_t = __shfl(s_t, lane > 0 ? lane - 1 : 0, 64);
+  uint64_t heads = __ballot(lane < nrouted && (lane == 0 || prev_t != s_t));
+  const int s_e = e0 + src;
+
+  uint64_t written = 0;   // kept slots (bucket-relative) already stored
+  while (heads) {         // one target slot per iteration, in ascending slot order
+    const int s0 = __builtin_ctzll(heads);
+    heads &= heads - 1;
+    const int s1 = heads ? __builtin_ctzll(heads) : nrouted;
+    const int k = __builtin_amdgcn_readlane(s_t, s0);
+    const int ki = k - k0;
+    const int tpos = __builtin_amdgcn_readlane(pos_k, ki);
+    const float a_t = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a_k), ki));
+    float vt[E];
+    load_slice<T, D>(Vh + (size_t)tpos * RB, col, vt);
+    const float vn_t = vnh[tpos];
+    float acc[E], kacc[MK ? E : 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < (MK ? E : 1); ++e) kacc[e] = 0.f;
+    float wsum = 0.f;
+    for (int ib0 = s0; ib0 < s1; ib0 += 4 * kBatch) {
+      int jj[kBatch], ev[kBatch];
+      float ajv[kBatch], vnjv[kBatch];
+      RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        const int sl = i < s1 ? i : s0;
+        jj[u] = __shfl(s_pos, sl, 64);
+        ajv[u] = __shfl(s_a, sl, 64);
+        vnjv[u] = __shfl(s_vn, sl, 64);
+        ev[u] = __shfl(s_e, sl, 64);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) vr[u].load(Vh + (size_t)jj[u] * RB, col);
+      if constexpr (MK) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) kre[u].load(Kh + (size_t)jj[u] * RB, col);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = ib0 + 4 * u + grp;
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
+        dot = sum16(dot);
+        float g = 0.f;
+        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
+          g = 1.f;
+        } else if (a.gate_mode == SELKV_GATE_COSINE) {
+          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
+          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
+        }
+        if (i < s1) {
+          const float w = g * ajv[u];
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
+          if constexpr (MK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) kacc[e] = fmaf(w, kre[u].get(e), kacc[e]);
+          }
+          wsum += w;
+          if (col == 0) gh[ev[u]] = g;
+        }
+      }
+    }
+    reduce_groups(acc);
+    if constexpr (MK) reduce_groups(kacc);
+    wsum += xor_shfl(wsum, 16);
+    wsum += xor_shfl(wsum, 32);
+    if (grp == 0) {
+      RawSlice<T, D> kr, vr;
+      kr.load(Kh + (size_t)tpos * RB, col);
+      vr.load(Vh + (size_t)tpos * RB, col);
+      if (wsum > 0.f) {
+        const float den = a_t + wsum;
+        RawSlice<T, D> mv;
+#pragma unroll
+        for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_t, vt[e], acc[e]) / den);
+        mv.store(Vo + (size_t)k * RB, col);
+        if constexpr (MK) {
+          RawSlice<T, D> mk;
+#pragma unroll
+          for (int e = 0; e < E; ++e) mk.put(e, fmaf(a_t, kr.get(e), kacc[e]) / den);
+          mk.store(Ko + (size_t)k * RB, col);
+        } else {
+          kr.store(Ko + (size_t)k * RB, col);
+        }
+      } else {
+        kr.store(Ko + (size_t)k * RB, col);
+        vr.store(Vo + (size_t)k * RB, col);
+      }
+    }
+    written |= 1ull << ki;
+  }
+  // the kept rows that absorbed nothing: copied bit for bit
+  for (int kb0 = 0; kb0 < nk; kb0 += 4 * kBatch) {
+    RawSlice<T, D> kr[kBatch], vr[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = kb0 + 4 * u + grp;
+      const int pos = __shfl(pos_k, i < nk ? i : 0, 64);
+      kr[u].load(Kh + (size_t)pos * RB, col);
+      vr[u].load(Vh + (size_t)pos * RB, col);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = kb0 + 4 * u + grp;
+      if (i < nk && !((written >> i) & 1ull)) {
+        kr[u].store(Ko + (size_t)(k0 + i) * RB, col);
+        vr[u].store(Vo + (size_t)(k0 + i) * RB, col);
+      }
+    }
+  }
+}
+
 struct BiasArgs {
   const float* attn;
   const int32_t* kept;
@@ -656,6 +838,47 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
     else SELKV_MB(float, 64);
   }
 #undef SELKV_MB
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_targets(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
+                                const void* K, const void* V, const float* attn, const float* vnorm,
+                                const int32_t* kept, const int32_t* evicted, const int32_t* offs,
+                                const int32_t* target, void* K_out, void* V_out, float* gate, bool merge_keys,
+                                hipStream_t st) {
+  MergeArgs a{};
+  a.K = static_cast<const char*>(K);
+  a.V = static_cast<const char*>(V);
+  a.attn = attn;
+  a.vnorm = vnorm;
+  a.kept = kept;
+  a.evicted = evicted;
+  a.offs = offs;
+  a.K_out = static_cast<char*>(K_out);
+  a.V_out = static_cast<char*>(V_out);
+  a.target = const_cast<int32_t*>(target);   // read only by this kernel
+  a.gate = gate;
+  a.n = s.n;
+  a.m = s.m;
+  a.nb = s.nb;
+  a.B = bucket;
+  a.gate_mode = gate_mode;
+  a.tau = tau;
+  a.inv_temp = 1.f / temp;
+  const dim3 grid((s.nb + kWavesPerBlock - 1) / kWavesPerBlock, (unsigned)s.heads);
+#define SELKV_MT(T, D)                                                                                  \
+  do {                                                                                                  \
+    if (merge_keys) hipLaunchKernelGGL((merge_targets_kernel<T, D, true>), grid, dim3(kThreads), 0, st, a); \
+    else hipLaunchKernelGGL((merge_targets_kernel<T, D, false>), grid, dim3(kThreads), 0, st, a);           \
+  } while (0)
+  if (dtype == SELKV_BF16) {
+    if (s.d == 128) SELKV_MT(bf16_t, 128);
+    else SELKV_MT(bf16_t, 64);
+  } else {
+    if (s.d == 128) SELKV_MT(float, 128);
+    else SELKV_MT(float, 64);
+  }
+#undef SELKV_MT
   return hipGetLastError();
 }
 

@@ -845,9 +845,10 @@ ScorePlan plan_score(const Shape& s, int dtype) {
   return p;
 }
 
-hipError_t launch_score(const Shape& s, const ScorePlan& p, int dtype, float scale, const void* K, const void* V,
-                        const void* Qwin, float* score, float* attn, float* vnorm, int pool_kernel, void* ws,
-                        hipStream_t st) {
+namespace {
+
+ScoreArgs make_args(const Shape& s, const ScorePlan& p, float scale, const void* K, const void* V, const void* Qwin,
+                    float* attn, float* vnorm, void* ws) {
   ScoreArgs a{};
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);
@@ -868,6 +869,44 @@ hipError_t launch_score(const Shape& s, const ScorePlan& p, int dtype, float sca
   a.rpad = p.rpad;
   a.nrg = p.nrg;
   a.c2 = scale * kLog2e;
+  return a;
+}
+
+template <typename T, int D>
+void launch_rowstats_general(const Shape& s, const ScorePlan& p, const ScoreArgs& a, hipStream_t st) {
+  const dim3 grid(p.nchunks, (unsigned)s.heads, p.nrg), blk(kThreads);
+  switch (p.rows_per_group) {
+    case 16: hipLaunchKernelGGL((score_rowstats_kernel<T, D, 1, 1>), grid, blk, 0, st, a); break;
+    case 32: hipLaunchKernelGGL((score_rowstats_kernel<T, D, 2, 1>), grid, blk, 0, st, a); break;
+    case 64: hipLaunchKernelGGL((score_rowstats_kernel<T, D, 4, 1>), grid, blk, 0, st, a); break;
+    default: hipLaunchKernelGGL((score_rowstats_kernel<T, D, 4, 2>), grid, blk, 0, st, a); break;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_row_stats(const Shape& s, const ScorePlan& p, int dtype, float scale, const void* K,
+                            const void* Qwin, void* ws, hipStream_t st) {
+  const ScoreArgs a = make_args(s, p, scale, K, nullptr, Qwin, nullptr, nullptr, ws);
+  if (dtype == SELKV_BF16 && p.tiled) {
+    if (s.d == 128) hipLaunchKernelGGL(score_rowstats_tiled<128>, dim3(p.nchunks, (unsigned)s.heads), dim3(kThreads),
+                                       0, st, a);
+    else hipLaunchKernelGGL(score_rowstats_tiled<64>, dim3(p.nchunks, (unsigned)s.heads), dim3(kThreads), 0, st, a);
+  } else if (dtype == SELKV_BF16) {
+    if (s.d == 128) launch_rowstats_general<bf16_t, 128>(s, p, a, st);
+    else launch_rowstats_general<bf16_t, 64>(s, p, a, st);
+  } else {
+    if (s.d == 128) launch_rowstats_general<float, 128>(s, p, a, st);
+    else launch_rowstats_general<float, 64>(s, p, a, st);
+  }
+  hipLaunchKernelGGL(score_combine_kernel, dim3((unsigned)s.heads), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const Shape& s, const ScorePlan& p, int dtype, float scale, const void* K, const void* V,
+                        const void* Qwin, float* score, float* attn, float* vnorm, int pool_kernel, void* ws,
+                        hipStream_t st) {
+  ScoreArgs a = make_args(s, p, scale, K, V, Qwin, attn, vnorm, ws);
   if (dtype == SELKV_BF16 && p.tiled) {
     if (s.d == 128) return launch_tiled<128>(s, p, a, score, pool_kernel, st);
     return launch_tiled<64>(s, p, a, score, pool_kernel, st);

@@ -29,7 +29,7 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
   if (!(p->gate_temperature > 0.f) || !isfinite(p->gate_temperature) || !isfinite(p->gate_threshold))
     return SELKV_EINVAL;
   if (p->gate_mode < SELKV_GATE_COSINE || p->gate_mode > SELKV_GATE_MERGE_ALL) return SELKV_EINVAL;
-  if (p->route_mode < SELKV_ROUTE_BUCKET || p->route_mode > SELKV_ROUTE_BUCKET_NEAREST) return SELKV_EINVAL;
+  if (p->route_mode < SELKV_ROUTE_BUCKET || p->route_mode > SELKV_ROUTE_COATTN) return SELKV_EINVAL;
   if (p->merge_keys != 0 && p->merge_keys != 1) return SELKV_EINVAL;
   if (p->select_mode != SELKV_SELECT_PER_HEAD && p->select_mode != SELKV_SELECT_UNION) return SELKV_EINVAL;
   const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
@@ -68,6 +68,11 @@ size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 // the grouping by target slot under full-cosine routing
 size_t merge_bytes(const selkv_params* p, const Shape& s) {
   return p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
+}
+
+// co-attention routing workspace: the score pass's row statistics, then the bucket offsets
+size_t route_bytes(const selkv_params* p, const Shape& s) {
+  return round256(plan_score(s, p->kv_dtype).bytes) + bucket_offsets_bytes(s);
 }
 
 // bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
@@ -134,6 +139,7 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
     case SELKV_CALL_SCORE: *bytes = plan_score(s, p->kv_dtype).bytes; return SELKV_OK;
     case SELKV_CALL_SELECT: *bytes = is_union(p) ? plan_union(s).select_bytes : 0; return SELKV_OK;
     case SELKV_CALL_MERGE: *bytes = merge_bytes(p, s); return SELKV_OK;
+    case SELKV_CALL_ROUTE: *bytes = route_bytes(p, s); return SELKV_OK;
     case SELKV_CALL_BIAS:
       *bytes = bias_base_bytes(p, s);
       if (is_union(p)) *bytes = round256(*bytes) + plan_union(s).ratio_bytes;
@@ -173,6 +179,31 @@ SELKV_API selkv_status selkv_select(const selkv_params* p, const float* score, i
   return hip_status(launch_select(s, score, kept_idx, evicted_idx, stream));
 }
 
+SELKV_API selkv_status selkv_route_coattn(const selkv_params* p, const void* K, const void* Qwin,
+                                          const int32_t* kept_idx, const int32_t* evicted_idx, int32_t* target,
+                                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  const bool has_ev = s.n > s.m;
+  if (!K || !Qwin || !kept_idx) return SELKV_EINVAL;
+  if (has_ev && (!evicted_idx || !target)) return SELKV_EINVAL;
+  if (!aligned(K, 16) || !aligned(Qwin, 16) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) ||
+      !aligned(target, 4))
+    return SELKV_EALIGN;
+  if ((st = check_ws(ws, ws_bytes, route_bytes(p, s))) != SELKV_OK) return st;
+  if (!has_ev) return SELKV_OK;
+  const ScorePlan sp = plan_score(s, p->kv_dtype);
+  int32_t* offs = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + round256(sp.bytes));
+  const float scale = eff_scale(p);
+  hipError_t e = launch_row_stats(s, sp, p->kv_dtype, scale, K, Qwin, ws, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  return hip_status(launch_coattn_route(s, sp, p->kv_dtype, p->bucket, p->window, K, Qwin, ws, kept_idx, offs, target,
+                                        scale * 1.4426950408889634f, stream));   // log2(e): logits in the log2 domain
+}
+
 SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const void* V, const float* attn,
                                    const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx,
                                    void* K_out, void* V_out, int32_t* target, float* gate, void* ws,
@@ -190,6 +221,15 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
   if ((st = check_ws(ws, ws_bytes, merge_bytes(p, s))) != SELKV_OK) return st;
   const bool mk = p->merge_keys != 0;
   hipError_t e;
+  if (p->route_mode == SELKV_ROUTE_COATTN) {
+    // targets given by selkv_route_coattn: grouped by target inside each bucket
+    int32_t* offs = static_cast<int32_t*>(ws);
+    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    return hip_status(launch_merge_targets(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
+                                           p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs,
+                                           target, K_out, V_out, gate, mk, stream));
+  }
   if (p->route_mode != SELKV_ROUTE_FULL_COSINE) {
     // bucket routings: one wave per bucket (plus its runs of empty buckets under the nearest-kept fallback)
     int32_t* offs = static_cast<int32_t*>(ws);

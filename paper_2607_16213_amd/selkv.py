@@ -18,14 +18,15 @@ LIB_PATH = os.path.join(_PKG, "libselkv.so")
 
 F32, BF16 = 0, 1
 GATE_COSINE, GATE_DROP, GATE_MERGE_ALL = 0, 1, 2
-ROUTE_BUCKET, ROUTE_FULL_COSINE, ROUTE_BUCKET_NEAREST = 0, 1, 2
+ROUTE_BUCKET, ROUTE_FULL_COSINE, ROUTE_BUCKET_NEAREST, ROUTE_COATTN = 0, 1, 2, 3
 SELECT_PER_HEAD, SELECT_UNION = 0, 1
-ABI_VERSION = 3
-CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE = range(5)
+ABI_VERSION = 4
+CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE, CALL_ROUTE = range(6)
 STATUS = {0: "SELKV_OK", 1: "SELKV_EINVAL", 2: "SELKV_EDTYPE", 3: "SELKV_EUNSUPPORTED", 4: "SELKV_EALIGN",
           5: "SELKV_EWORKSPACE", 6: "SELKV_EHIP"}
 GATE_MODES = {"cosine": GATE_COSINE, "drop": GATE_DROP, "merge_all": GATE_MERGE_ALL}
-ROUTE_MODES = {"bucket": ROUTE_BUCKET, "full_cosine": ROUTE_FULL_COSINE, "bucket_nearest": ROUTE_BUCKET_NEAREST}
+ROUTE_MODES = {"bucket": ROUTE_BUCKET, "full_cosine": ROUTE_FULL_COSINE, "bucket_nearest": ROUTE_BUCKET_NEAREST,
+               "coattn": ROUTE_COATTN}
 SELECT_MODES = {"per_head": SELECT_PER_HEAD, "union": SELECT_UNION}
 
 
@@ -72,6 +73,7 @@ def _load():
         "selkv_workspace_size": (ctypes.c_int, [P, i32, i32, ctypes.POINTER(sz)]),
         "selkv_score": (ctypes.c_int, [P, vp, vp, vp, fp, fp, fp, vp, sz, vp]),
         "selkv_select": (ctypes.c_int, [P, fp, ip, ip, vp, sz, vp]),
+        "selkv_route_coattn": (ctypes.c_int, [P, vp, vp, ip, ip, ip, vp, sz, vp]),
         "selkv_merge": (ctypes.c_int, [P, vp, vp, fp, fp, ip, ip, vp, vp, ip, fp, vp, sz, vp]),
         "selkv_bias": (ctypes.c_int, [P, fp, ip, ip, ip, fp, fp, vp, sz, vp]),
         "selkv_decode_attn": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp, sz, vp]),
@@ -181,6 +183,19 @@ def select(p, score_in, kept, evicted, ws=None, stream=None):
                             ws.numel() if ws is not None else 0, _stream(stream)), "selkv_select")
 
 
+def route_coattn(p, K, Qwin, kept, evicted, target, ws, stream=None):
+    """Co-attention routing (route_mode COATTN): target slots for selkv_merge / selkv_bias."""
+    B, H, n, d = p.batch, p.n_heads_kv, p.seq_len, p.head_dim
+    m, mr, ms = budget(p)
+    dt = _kvdt(p)
+    _dev(K, (B, H, n, d), dt, "K"); _dev(Qwin, (B, H * p.group, p.window, d), dt, "Qwin")
+    _dev(kept, (B, H, m), torch.int32, "kept_idx"); _dev(evicted, (B, H, n - m), torch.int32, "evicted_idx")
+    _dev(target, (B, H, n - m), torch.int32, "target")
+    _check(lib.selkv_route_coattn(ctypes.byref(p), _ptr(K), _ptr(Qwin), _ptr(kept), _ptr(evicted), _ptr(target),
+                                  _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
+           "selkv_route_coattn")
+
+
 def merge(p, K, V, attn, vnorm, kept, evicted, K_out, V_out, target, gate, ws, stream=None):
     B, H, n, d = p.batch, p.n_heads_kv, p.seq_len, p.head_dim
     m, mr, ms = budget(p)
@@ -248,7 +263,7 @@ def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=
 
 class Compressor:
     """Owns the output and scratch tensors of one problem size and runs the
-    four compression calls (score, select, merge, bias) on the current
+    compression calls (score, select, [route_coattn,] merge, bias) on the current
     stream.  Allocation happens once, in the constructor."""
 
     def __init__(self, p: Params, device):
@@ -272,11 +287,14 @@ class Compressor:
         self.ws_select = workspace(p, CALL_SELECT, device)
         self.ws_merge = workspace(p, CALL_MERGE, device)
         self.ws_bias = workspace(p, CALL_BIAS, device)
+        self.ws_route = workspace(p, CALL_ROUTE, device) if p.route_mode == ROUTE_COATTN else None
 
     def run(self, K, V, Qwin, stream=None):
         p = self.p
         score(p, K, V, Qwin, self.score, self.attn, self.vnorm, self.ws_score, stream)
         select(p, self.score, self.kept, self.evicted, self.ws_select, stream)
+        if p.route_mode == ROUTE_COATTN:
+            route_coattn(p, K, Qwin, self.kept, self.evicted, self.target, self.ws_route, stream)
         merge(p, K, V, self.attn, self.vnorm, self.kept, self.evicted, self.K_out, self.V_out, self.target,
               self.gate, self.ws_merge, stream)
         bias(p, self.attn, self.kept, self.evicted, self.target, self.gate, self.bias, self.ws_bias, stream)

@@ -63,7 +63,7 @@ def test_params_init_defaults(S):
     assert p.struct_size == ctypes.sizeof(S.Params)
     assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
     assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
-    assert S.lib.selkv_abi_version() == 3
+    assert S.lib.selkv_abi_version() == 4
     assert S.lib.selkv_status_string(0) == b"success"
 
 
@@ -165,7 +165,7 @@ def test_alternative_readings_validation_and_workspace(S):
     """Nearest-kept fallback and key merging: the flags are checked, and both
     stay bucket-local (the workspace of the plain bucket routing)."""
     b = ctypes.c_size_t()
-    for bad in (S.params(seq_len=256, route_mode=3), S.params(seq_len=256, route_mode=-1),
+    for bad in (S.params(seq_len=256, route_mode=4), S.params(seq_len=256, route_mode=-1),
                 S.params(seq_len=256, merge_keys=2)):
         assert S.lib.selkv_workspace_size(ctypes.byref(bad), S.CALL_MERGE, 0, ctypes.byref(b)) == 1
     plain = S.params(seq_len=256)
@@ -176,3 +176,27 @@ def test_alternative_readings_validation_and_workspace(S):
         assert S.workspace_bytes(full, call) > S.workspace_bytes(plain, call)
     keys = S.params(seq_len=256, merge_keys=1)
     assert S.workspace_bytes(keys, S.CALL_MERGE) == S.workspace_bytes(plain, S.CALL_MERGE)
+
+
+def test_coattn_route_validation_and_workspace(S):
+    """Co-attention routing: the route mode is accepted, its workspace holds
+    the score pass's row statistics plus the bucket offsets, and the call
+    checks its arguments before any launch."""
+    p = S.params(seq_len=4096, route_mode="coattn")
+    assert S.workspace_bytes(p, S.CALL_ROUTE) >= S.workspace_bytes(p, S.CALL_SCORE) - 4 * 8 * 4096
+    assert S.workspace_bytes(p, S.CALL_MERGE) == S.workspace_bytes(S.params(seq_len=4096), S.CALL_MERGE)
+    b = ctypes.c_size_t()
+    bad = S.params(seq_len=256, route_mode=4)
+    assert S.lib.selkv_workspace_size(ctypes.byref(bad), S.CALL_ROUTE, 0, ctypes.byref(b)) == 1
+    assert S.lib.selkv_workspace_size(ctypes.byref(p), 6, 0, ctypes.byref(b)) == 1
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_coattn_route_call_validation(S):
+    p = S.params(seq_len=256, route_mode="coattn")
+    fake, mis = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10004)
+    f = S.lib.selkv_route_coattn
+    assert f(ctypes.byref(p), None, fake, fake, fake, fake, fake, 1 << 30, None) == 1
+    assert f(ctypes.byref(p), fake, fake, fake, None, fake, fake, 1 << 30, None) == 1        # evicted needed
+    assert f(ctypes.byref(p), fake, mis, fake, fake, fake, fake, 1 << 30, None) == 4         # Qwin 16-byte aligned
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 64, None) == 5             # workspace too small

@@ -852,3 +852,131 @@ def test_nearest_fallback_end_to_end_llama_layer(S):
     routed = tp >= 0
     assert (~routed).any(), "a 10% budget with bucket 8 must leave empty buckets"
     np.testing.assert_array_equal(tn[routed], tp[routed])
+
+
+# ------------------------------------------------------------------ co-attention routing (alternative reading of Eq. 3)
+COATTN = [
+    dict(batch=1, H=2, G=2, d=64, n=500, W=16, dtype="fp32"),
+    dict(batch=2, H=1, G=4, d=128, n=1000, W=32, dtype="bf16"),                      # shared-tile row statistics
+    dict(batch=1, H=2, G=4, d=128, n=700, W=16, dtype="bf16", bucket=64, budget_ratio=0.1),
+    dict(batch=1, H=1, G=3, d=64, n=333, W=8, dtype="bf16", bucket=20, gate_mode=2, merge_keys=1),
+    dict(batch=1, H=1, G=8, d=64, n=600, W=32, dtype="bf16", bucket=8),              # 256 rows: general passes
+    dict(batch=1, H=2, G=2, d=128, n=400, W=8, dtype="fp32", bucket=16, budget_ratio=0.05, gate_mode=1),
+    dict(batch=1, H=1, G=2, d=64, n=200, W=8, dtype="fp32", budget_ratio=1.0),       # nothing evicted
+]
+COATTN_NEAR_TIE = 1e-4   # relative gap of two co-attentions below which fp32 may pick either
+
+
+@pytest.mark.parametrize("case", COATTN, ids=[f"coattn{i}" for i in range(len(COATTN))])
+def test_coattn_routing_stagewise(S, case):
+    """Co-attention routing fed the oracle's kept / evicted lists: every
+    target equals the oracle's argmax of sum_r A[r, j] A[r, i] (float64 A)
+    except where the two candidates' co-attentions lie within 1e-4 of each
+    other relative (counted).  Merge and bias with route_mode COATTN are then
+    fed the oracle's targets: gates, merged values (and keys), gathered keys
+    and the bias as for the bucket routing."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 13 + 5, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=6, device=DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case, route_mode="coattn", **kw)
+    mk = bool(p.merge_keys)
+    tol = TOL[case["dtype"]]
+    B, H, n, d = K.shape
+    G = p.group
+    m, mr, ms = S.budget(p)
+    comp = S.Compressor(p, DEV)
+    S.score(p, K, V, Q, comp.score, comp.attn, comp.vnorm, comp.ws_score)
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(K), np64(V), np64(Q)
+    a_in, vn_in = comp.attn.clone(), comp.vnorm.clone()
+    refs = {}
+    for b in range(B):
+        for h in range(H):
+            ch = oracle_chain(K64[b, h], V64[b, h], Q64[b, h * G:(h + 1) * G], p, GATE[p.gate_mode])
+            comp.kept[b, h] = torch.as_tensor(ch["kept"], dtype=torch.int32)
+            comp.evicted[b, h] = torch.as_tensor(ch["ev"], dtype=torch.int32)
+            a_in[b, h] = torch.as_tensor(ch["a32"], dtype=torch.float32)
+            vn_in[b, h] = torch.as_tensor(ch["vn"], dtype=torch.float32)
+            A = O.window_attention_group(Q64[b, h * G:(h + 1) * G], K64[b, h], oracle_scale(p))
+            refs[(b, h)] = dict(ch=ch, A=A, target=O.route_coattention(A, ch["kept"], ch["ev"], p.bucket))
+    comp.target.fill_(-7)
+    S.route_coattn(p, K, Q, comp.kept, comp.evicted, comp.target, comp.ws_route)
+    torch.cuda.synchronize()
+    ties = 0
+    for (b, h), r in refs.items():
+        ch, A, tg_ref = r["ch"], r["A"], r["target"]
+        tg = comp.target[b, h].cpu().numpy()
+        np.testing.assert_array_equal(tg < 0, tg_ref < 0, err_msg="empty buckets")
+        for e in np.flatnonzero(tg != tg_ref):
+            j = ch["ev"][e]
+            co = lambda s: float(A[:, ch["kept"][s]] @ A[:, j])
+            c_gpu, c_ref = co(tg[e]), co(tg_ref[e])
+            assert ch["kept"][tg[e]] // p.bucket == j // p.bucket, "target outside the bucket"
+            assert abs(c_gpu - c_ref) <= COATTN_NEAR_TIE * abs(c_ref), f"routing differs at evicted {e}"
+            ties += 1
+    # merge / bias fed the oracle's targets
+    for (b, h), r in refs.items():
+        ch, tg = r["ch"], r["target"]
+        comp.target[b, h] = torch.as_tensor(tg, dtype=torch.int32)
+        g = O.gate(V64[b, h], ch["kept"], ch["ev"], tg, GATE[p.gate_mode], float(np.float32(p.gate_threshold)),
+                   float(np.float32(p.gate_temperature)))
+        r["g"] = g
+        r["g32"] = g.astype(np.float32).astype(np.float64)
+        r["k_out"], r["v_out"], _ = O.merge(K64[b, h], V64[b, h], ch["a32"], ch["kept"], ch["ev"], tg, g,
+                                            merge_keys=mk)
+        r["bias"] = O.ratio_bias(ch["a32"], ch["kept"], ch["ev"], tg, r["g32"], float(np.float32(p.alpha)))
+    t_in = comp.target.clone()
+    S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
+            comp.ws_merge)
+    torch.cuda.synchronize()
+    assert torch.equal(comp.target, t_in), "merge must not write the given targets"
+    for (b, h), r in refs.items():
+        ch = r["ch"]
+        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert_close_rows(np64(comp.V_out[b, h]), r["v_out"], tol, f"V_out[{b},{h}]")
+        if mk:
+            assert_close_rows(np64(comp.K_out[b, h]), r["k_out"], tol, f"K_out[{b},{h}]")
+        else:
+            assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(ch["kept"])]), f"K_out[{b},{h}]"
+        untouched = np.setdiff1d(np.arange(m), r["target"][r["target"] >= 0])
+        sel = torch.as_tensor(untouched, dtype=torch.long)
+        assert torch.equal(comp.V_out[b, h].cpu()[sel], V[b, h].cpu()[torch.as_tensor(ch["kept"][untouched])])
+        comp.gate[b, h] = torch.as_tensor(r["g32"], dtype=torch.float32)
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    torch.cuda.synchronize()
+    for (b, h), r in refs.items():
+        err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
+        assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
+    print(f"co-attention routing near-ties: {ties}")
+
+
+def test_coattn_end_to_end_llama_layer(S):
+    """The whole pipeline with co-attention routing on a Llama-shaped layer:
+    every target lies in its token's bucket, -1 exactly for the buckets that
+    keep nothing, at least one bucket routes differently from Eq. 3, and the
+    run is bitwise repeatable."""
+    w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096, n_heads_kv=4)
+    t = synth.make_layer(w, 0, DEV)
+    p_co = make_params(S, case_from_workload(w), route_mode="coattn")
+    p_eq3 = make_params(S, case_from_workload(w))
+    outs = []
+    for p in (p_co, p_co, p_eq3):
+        c = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+        torch.cuda.synchronize()
+        outs.append({k: v.clone() for k, v in c.outputs().items()})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    co, eq3 = outs[0], outs[2]
+    assert torch.equal(co["kept"], eq3["kept"])
+    kept, ev = co["kept"].cpu().numpy(), co["evicted"].cpu().numpy()
+    tc, te = co["target"].cpu().numpy(), eq3["target"].cpu().numpy()
+    np.testing.assert_array_equal(tc < 0, te < 0)
+    Bk = p_co.bucket
+    for b in range(kept.shape[0]):
+        for h in range(kept.shape[1]):
+            ok = tc[b, h] >= 0
+            assert (kept[b, h][tc[b, h][ok]] // Bk == ev[b, h][ok] // Bk).all()
+    assert (tc != te).any(), "co-attention should route some token differently from Eq. 3"
