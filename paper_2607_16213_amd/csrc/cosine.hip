@@ -156,15 +156,21 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
 }
 
 // bf16 variant with the kept rows shared through LDS.  A workgroup holds 256
-// evicted rows (64 per wave, the MFMA A operand in registers) and streams the
-// head's kept rows in tiles of 64: each thread gathers 1/256 of a tile with
-// 16-byte loads, kMatchDepth tiles ahead, the kept positions one lap further
-// ahead still, and stores it XOR-swizzled into one of two LDS stages that all
-// four waves read as the B operand.  The running argmax compares
+// evicted rows (64 per wave, in registers) and streams the head's kept rows
+// in tiles of 64 through two LDS stages that all four waves read.  The tiles
+// are gathered straight into LDS by 16-byte LDS-DMA loads (no register
+// staging): a wave's load fills 1 KB of LDS in lane order, so each lane picks
+// the kept row and 16-byte chunk whose XOR-swizzled place is its own slot.
+// Only the kept positions (one tile ahead) and one norm pass through
+// registers, which keeps the kernel at three waves per SIMD.  The kept tile
+// is the MFMA A operand and the evicted rows the B operand, so lane (g, c)
+// receives slots 4g .. 4g+3 of a 16-slot block for evicted row c: its four
+// candidates for one row.  The running argmax takes their maximum with the
+// running best (two max3) and looks up which slot it was only when the best
+// improves, which becomes rare along the stream.  It compares
 // dot * (1 / ||v_i||) only: the evicted row's own norm does not change its
 // argmax and is applied once, to the winner, for the gate.
 constexpr int kMT = 64;          // kept rows per tile
-constexpr int kMatchDepth = 2;   // tiles of loads in flight per thread
 constexpr int kMatchTiledRB = 4; // 16-row blocks of evicted rows per wave
 
 template <int D>
@@ -173,29 +179,35 @@ struct MGeo {
   static constexpr int NCHUNK = RB / 16;
   static constexpr int NCH = RB / 64;
   static constexpr int TILE = kMT * RB;
-  static constexpr int LPT = TILE / (kThreads * 16);
+  static constexpr int LPT = TILE / (kThreads * 16);   // LDS-DMA loads per thread per tile
   static_assert(LPT >= 1 && TILE % (kThreads * 16) == 0, "tile must split evenly over the workgroup");
 };
-
-template <int D>
-__device__ __forceinline__ void mpiece(int j, int tid, int& row, int& ch) {
-  const int off = (j * kThreads + tid) * 16;
-  row = off / MGeo<D>::RB;
-  ch = (off % MGeo<D>::RB) / 16;
-}
 
 template <int D>
 __device__ __forceinline__ int mswz(int row, int ch) {
   return row * MGeo<D>::RB + ((ch ^ (row & (MGeo<D>::NCHUNK - 1))) * 16);
 }
 
+// The LDS bytes that load j of wave w fills: [(j * kWaves + w) * 1024, + 1024),
+// lane L at + 16 L.  Returns the tile row and the (unswizzled) chunk whose
+// swizzled place that is.
 template <int D>
-__global__ __launch_bounds__(kThreads) void cosine_match_tiled(MatchArgs a) {
+__device__ __forceinline__ void dma_piece(int j, int wave, int lane, int& row, int& ch) {
+  const int p = (j * kWaves + wave) * 1024 + lane * 16;
+  row = p / MGeo<D>::RB;
+  ch = ((p % MGeo<D>::RB) / 16) ^ (row & (MGeo<D>::NCHUNK - 1));
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   using Geo = MGeo<D>;
   constexpr int NCH = Geo::NCH, LPT = Geo::LPT, NRB = kMatchTiledRB;
-  __shared__ __align__(16) char lds[2][Geo::TILE];
-  __shared__ float s_inv[2][kMT];    // 1 / ||v_i|| of the tile's kept rows
-  __shared__ float s_off[2][kMT];    // 0, or -inf past the last kept slot
+  // two stages as separate arrays, addressed statically (the tile loop is
+  // unrolled by two), so that reading one stage never waits for the loads
+  // still filling the other
+  __shared__ __align__(16) char lds0[Geo::TILE], lds1[Geo::TILE];
+  __shared__ __align__(16) float s_inv0[kMT], s_inv1[kMT];   // 1 / ||v_i|| of the tile's kept rows
+  __shared__ __align__(16) float s_off0[kMT], s_off1[kMT];   // 0, or -inf past the last kept slot
   const int64_t head = blockIdx.y;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -214,153 +226,144 @@ __global__ __launch_bounds__(kThreads) void cosine_match_tiled(MatchArgs a) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) q[rb][c] = load16(Vh + (size_t)pos * Geo::RB + (c * 4 + grp) * 16);
   }
-  float best[NRB][4];
-  int bidx[NRB][4];
+  float best[NRB];   // evicted row rb*16 + col, over the slots 4g .. 4g+3 of every block
+  int bidx[NRB];
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      best[rb][i] = kNegInf;
-      bidx[rb][i] = 0;
-    }
+  for (int rb = 0; rb < NRB; ++rb) {
+    best[rb] = kNegInf;
+    bidx[rb] = 0;
+  }
 
   const int ntiles = (m + kMT - 1) / kMT;
-  // register rings: kept positions (one lap ahead of the data), data, norms
-  int ix[kMatchDepth][LPT], ixn[kMatchDepth];
-  Chunk16 rk[kMatchDepth][LPT];
-  float rn[kMatchDepth];
+  int ix[2][LPT];      // kept positions of this thread's DMA rows, one tile ahead
+  int ixn[2];          // kept position of slot tid & (kMT - 1) (its norm), one tile ahead
+  float rn = 0.f;
   auto load_pos = [&](int slot, int tile) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
       int row, ch;
-      mpiece<D>(j, tid, row, ch);
+      dma_piece<D>(j, wave, lane, row, ch);
       ix[slot][j] = kh[min(tile * kMT + row, m - 1)];
     }
     ixn[slot] = kh[min(tile * kMT + (tid & (kMT - 1)), m - 1)];
   };
-  auto load_data = [&](int slot) {
+  // past the end the loads re-read the last kept row (masked by s_off), so
+  // every trip issues the same loads
+  auto issue_tile = [&](int slot, char* stage) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
       int row, ch;
-      mpiece<D>(j, tid, row, ch);
-      rk[slot][j] = load16(Vh + (size_t)ix[slot][j] * Geo::RB + ch * 16);
+      dma_piece<D>(j, wave, lane, row, ch);
+      __builtin_amdgcn_global_load_lds(
+          static_cast<const void*>(Vh + (size_t)ix[slot][j] * Geo::RB + ch * 16),
+          (__attribute__((address_space(3))) void*)(stage + (j * kWaves + wave) * 1024), 16, 0, 0);
     }
-    rn[slot] = vnh[ixn[slot]];
+    rn = vnh[ixn[slot]];
   };
-  auto commit = [&](int slot, int stage, int tile) {
-#pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      int row, ch;
-      mpiece<D>(j, tid, row, ch);
-      store16(lds[stage] + mswz<D>(row, ch), rk[slot][j]);
-    }
+  auto commit_norm = [&](float* sinv, float* soff, int tile) {
     if (tid < kMT) {
-      s_inv[stage][tid] = rn[slot] > 0.f ? 1.f / rn[slot] : 0.f;
-      s_off[stage][tid] = tile * kMT + tid < m ? 0.f : kNegInf;
+      sinv[tid] = rn > 0.f ? 1.f / rn : 0.f;
+      soff[tid] = tile * kMT + tid < m ? 0.f : kNegInf;
     }
   };
-  // value = fma(dot, 1 / ||v_i||, off): off = -inf masks slots past the end,
-  // so every tile runs the same branch-free code
+  // value = fma(dot, 1 / ||v_i||, off): off = -inf masks slots past the end
   // the MFMAs of column block kk + 1 are issued before the epilogue of block
   // kk, so the matrix core and the VALU work on independent data
-  auto mfma_block = [&](int stage, int kk, f32x4 (&acc)[NRB]) {
+  auto mfma_block = [&](const char* stage, int kk, f32x4 (&acc)[NRB]) {
     const int row = kk * 16 + col;
     Chunk16 bf[NCH];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) bf[c] = *reinterpret_cast<const Chunk16*>(lds[stage] + mswz<D>(row, c * 4 + grp));
+    for (int c = 0; c < NCH; ++c) bf[c] = *reinterpret_cast<const Chunk16*>(stage + mswz<D>(row, c * 4 + grp));
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) acc[rb] = Mma<bf16_t>::step(q[rb][c], bf[c], acc[rb]);
+      for (int c = 0; c < NCH; ++c) acc[rb] = Mma<bf16_t>::step(bf[c], q[rb][c], acc[rb]);
     }
   };
-  auto epilogue = [&](int stage, int tile, int kk, const f32x4 (&acc)[NRB]) {
-    const int row = kk * 16 + col;
-    const int slot = tile * kMT + row;
-    const float icur = s_inv[stage][row], off = s_off[stage][row];
+  auto epilogue = [&](const float* sinv, const float* soff, int tile, int kk, const f32x4 (&acc)[NRB]) {
+    const int s0 = kk * 16 + grp * 4;
+    const f32x4 inv = *reinterpret_cast<const f32x4*>(sinv + s0);
+    const f32x4 off = *reinterpret_cast<const f32x4*>(soff + s0);
+    const int slot0 = tile * kMT + s0;
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        // slots rise along the stream: a strict compare keeps the lower slot on ties
-        const float v = fmaf(acc[rb][i], icur, off);
-        const bool gt = v > best[rb][i];
-        best[rb][i] = gt ? v : best[rb][i];
-        bidx[rb][i] = gt ? slot : bidx[rb][i];
+    for (int rb = 0; rb < NRB; ++rb) {
+      const float v0 = fmaf(acc[rb][0], inv[0], off[0]);
+      const float v1 = fmaf(acc[rb][1], inv[1], off[1]);
+      const float v2 = fmaf(acc[rb][2], inv[2], off[2]);
+      const float v3 = fmaf(acc[rb][3], inv[3], off[3]);
+      const float mx = fmaxf(fmaxf(best[rb], v0), fmaxf(fmaxf(v1, v2), v3));
+      // slots rise along the stream: only a strictly larger value moves the
+      // best, and the lowest of the four slots holding it is taken
+      if (mx > best[rb]) {
+        bidx[rb] = v0 == mx ? slot0 : v1 == mx ? slot0 + 1 : v2 == mx ? slot0 + 2 : slot0 + 3;
+        best[rb] = mx;
       }
+    }
   };
-  auto body = [&](int stage, int tile) {
+  auto body = [&](const char* stage, const float* sinv, const float* soff, int tile) {
     f32x4 acc[2][NRB];
     mfma_block(stage, 0, acc[0]);
 #pragma unroll
     for (int kk = 0; kk < kMT / 16; ++kk) {
       if (kk + 1 < kMT / 16) mfma_block(stage, kk + 1, acc[(kk + 1) & 1]);
-      epilogue(stage, tile, kk, acc[kk & 1]);
+      epilogue(sinv, soff, tile, kk, acc[kk & 1]);
     }
   };
+  // trip t: the other stage was released by the last barrier, so tile t+1 is
+  // gathered into it while tile t is used; the barrier at the end waits for
+  // every load of the trip, issued a whole tile body earlier
+  auto trip = [&](int cur, char* Lc, float* ic, float* oc, char* Ln, float* in_, float* on, int t) {
+    issue_tile(cur ^ 1, Ln);
+    load_pos(cur, t + 2);
+    body(Lc, ic, oc, t);
+    commit_norm(in_, on, t + 1);
+    __syncthreads();
+  };
 
-  // prologue: positions for tiles 0 .. 2*depth-1, data for tiles 0 .. depth-1
-#pragma unroll
-  for (int p = 0; p < kMatchDepth; ++p) load_pos(p, p);
-#pragma unroll
-  for (int p = 0; p < kMatchDepth; ++p) load_data(p);
-#pragma unroll
-  for (int p = 0; p < kMatchDepth; ++p) load_pos(p, p + kMatchDepth);
-  commit(0, 0, 0);
-  load_data(0);
-  load_pos(0, 2 * kMatchDepth);
+  // prologue: tile 0 in stage 0, positions of tile 1
+  load_pos(0, 0);
+  issue_tile(0, lds0);
+  load_pos(1, 1);
+  commit_norm(s_inv0, s_off0, 0);
   __syncthreads();
-  // every load, LDS store and tile body runs on every trip: past the end the
-  // loads re-read the last kept row and the masks turn those slots to -inf,
-  // so the loop has no branches and the compiler waits only for the oldest slot
-  for (int i = 0; i < ntiles; i += kMatchDepth) {
-#pragma unroll
-    for (int u = 0; u < kMatchDepth; ++u) {
-      const int tile = i + u;
-      const int nu = (u + 1) % kMatchDepth;    // a constant once the loop is unrolled
-      commit(nu, (tile + 1) & 1, tile + 1);
-      load_data(nu);
-      load_pos(nu, tile + 1 + 2 * kMatchDepth);
-      body(tile & 1, tile);
-      __syncthreads();
-    }
+  // two trips per pass; an odd tile count runs one trip past the end, whose
+  // slots s_off masks to -inf (its loads re-read the last kept row)
+  for (int t = 0; t < ntiles; t += 2) {
+    trip(0, lds0, s_inv0, s_off0, lds1, s_inv1, s_off1, t);
+    trip(1, lds1, s_inv1, s_off1, lds0, s_inv0, s_off0, t + 1);
   }
 
   if (!active) return;
-  // merge the 16 lanes (slot subsets) of each row: larger value, then lower slot
+  // merge the four lane groups (slot subsets) of each row: larger value, then lower slot
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const float ob = xor_shfl(best[rb][i], off);
-        const int oi = xor_shfl(bidx[rb][i], off);
-        if (ob > best[rb][i] || (ob == best[rb][i] && oi < bidx[rb][i])) {
-          best[rb][i] = ob;
-          bidx[rb][i] = oi;
-        }
+    for (int off = 16; off < 64; off <<= 1) {
+      const float ob = xor_shfl(best[rb], off);
+      const int oi = xor_shfl(bidx[rb], off);
+      if (ob > best[rb] || (ob == best[rb] && oi < bidx[rb])) {
+        best[rb] = ob;
+        bidx[rb] = oi;
       }
-  if (col == 0) {
+    }
+  if (grp == 0) {
     int32_t* th = a.target + (size_t)head * ne;
     float* gh = a.gate + (size_t)head * ne;
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = r0 + rb * 16 + grp * 4 + i;
-        if (e < ne) {
-          const float vn = vnh[eh[e]];
-          const float cosv = vn > 0.f ? best[rb][i] * (1.f / vn) : 0.f;
-          float g;
-          if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
-          else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
-          else g = fminf(1.f, fmaxf(0.f, (cosv - a.tau) * a.inv_temp));
-          th[e] = bidx[rb][i];
-          gh[e] = g;
-        }
+    for (int rb = 0; rb < NRB; ++rb) {
+      const int e = r0 + rb * 16 + col;
+      if (e < ne) {
+        const float vn = vnh[eh[e]];
+        const float cosv = vn > 0.f ? best[rb] * (1.f / vn) : 0.f;
+        float g;
+        if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
+        else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
+        else g = fminf(1.f, fmaxf(0.f, (cosv - a.tau) * a.inv_temp));
+        th[e] = bidx[rb];
+        gh[e] = g;
       }
+    }
   }
 }
 
