@@ -40,7 +40,8 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload's)")
     ap.add_argument("--no-32k", action="store_true", help="skip the 32k-context secondary point")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=6, help="(layer, head) slices the oracle compresses")
+    ap.add_argument("--cpu-heads", type=int, default=18,
+                    help="(layer, head) slices the oracle compresses (about 10-15 s of CPU work)")
     ap.add_argument("--no-graph", action="store_true", help="launch decode eagerly instead of from a HIP graph")
     ap.add_argument("--print-source-hash", action="store_true", help="print the decode source hash and exit")
     ap.add_argument("--full-cosine-layers", type=int, default=1,
