@@ -307,12 +307,14 @@ SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, c
                                          size_t ws_bytes, hipStream_t stream);
 
 /* One generation step over a cache that grows (the decode loop after
- * compression, Sec. 4.4): the new token's key and value are written at
- * entry cache_len of every KV head, with bias 0 there when bias is given
- * (a new token absorbed nothing, so R = 1), and then the step attends over
- * the cache_len + 1 entries exactly as selkv_decode_attn.
- * In:  q [B, H_kv*G, d]; k_new, v_new [B, H_kv, d] (kv_dtype);
- *      0 <= cache_len < capacity.
+ * compression, Sec. 4.4): the step attends over the cache_len + 1 entries
+ * exactly as selkv_decode_attn, the last one being the new token, whose
+ * key and value it reads from k_new / v_new with bias 0 (a new token
+ * absorbed nothing, so R = 1).  The same launch stores them at entry
+ * cache_len of every KV head (and bias 0 there when bias is given) for the
+ * later steps.
+ * In:  q [B, H_kv*G, d]; k_new, v_new [B, H_kv, d] (kv_dtype; must not
+ *      overlap the cache); 0 <= cache_len < capacity.
  * In/out: K, V [B, H_kv, capacity, d] (entries past cache_len + 1 are not
  *      read); bias [B, H_kv, capacity] fp32 or NULL.
  * Out: out [B, H_kv*G, d] fp32.

@@ -15,6 +15,10 @@
 // cross-workgroup hand-off inside one kernel would need device-scope cache
 // write-back / invalidate on every workgroup, and on a multi-XCD device that
 // costs more than the second launch.  Deterministic.
+// Appending (selkv_decode_append): the last entry is read from the caller's
+// new key / value rows while the step runs, and the workgroup that owns it
+// also stores those rows into the cache, so a generation step is one launch
+// pair like any other decode step.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -126,9 +130,32 @@ struct DecodeArgs {
   int L, chunk, nsplit;
   int stride;       // entries between consecutive heads in K, V and bias (>= L)
   float c2;         // scale * log2(e)
+  // appended token (new_key = L - 1) or none (new_key = -1): its rows per
+  // head in k_new / v_new; the workgroup holding it also stores them (and a
+  // zero bias) into the cache through K_w / V_w / bias_w
+  const char* k_new;
+  const char* v_new;
+  char* K_w;
+  char* V_w;
+  float* bias_w;
+  int new_key;
 };
 
-template <typename T, int D, int G, bool BIAS>
+// Store the appended token's rows (and bias 0) into the cache: wave 0 of the
+// workgroup whose chunk holds it, at the end of the kernel.  Nothing else
+// reads those cache rows in this launch (they are read from k_new / v_new).
+template <int RB>
+__device__ __forceinline__ void store_new_row(const DecodeArgs& a, int64_t head, int split, int wave, int lane) {
+  if (a.new_key < 0 || split != a.new_key / a.chunk || wave != 0) return;
+  const size_t row = (size_t)head * a.stride + a.new_key;
+  for (int c = lane; c * 16 < RB; c += 64) {
+    store16(a.K_w + row * RB + c * 16, load16(a.k_new + (size_t)head * RB + c * 16));
+    store16(a.V_w + row * RB + c * 16, load16(a.v_new + (size_t)head * RB + c * 16));
+  }
+  if (a.bias_w && lane == 0) a.bias_w[row] = 0.f;
+}
+
+template <typename T, int D, int G, bool BIAS, bool APP>
 __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   constexpr int E = Slice<T, D>::kElems;
   constexpr int RB = D * (int)sizeof(T);
@@ -155,7 +182,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   }
 
   const int kb = split * a.chunk;
-  const int ke = min(L, kb + a.chunk);
+  // APP: the loop stops before the appended entry, which is taken below
+  const int ke = min(APP ? a.new_key : L, kb + a.chunk);
   // two register buffers: the loads of the next step are in flight while
   // the current one is computed (rows past the chunk end re-read the last
   // row of the chunk and are masked, so no load sits behind a branch)
@@ -172,6 +200,13 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     load_step<T, D, BIAS>(Kh, Vh, bh, base + stride, ke, grp, col, kA, vA, bA);
     attend_step<T, D, G>(q, a.c2, base, ke, grp, kB, vB, bB, mrun, lrun, o);
     base += stride;
+  }
+  // the appended entry: one masked step of wave 0 of the workgroup that owns
+  // it, reading the caller's rows (bias 0)
+  if (APP && wave == 0 && a.new_key >= kb && a.new_key < kb + a.chunk) {
+    load_step<T, D, false>(a.k_new + (size_t)head * RB, a.v_new + (size_t)head * RB, nullptr, 0, 1, grp, col, kA, vA,
+                           bA);
+    attend_step<T, D, G>(q, a.c2, 0, 1, grp, kA, vA, bA, mrun, lrun, o);
   }
 
   // merge the four lane groups of the wave (xor 16, then xor 32)
@@ -227,6 +262,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     po[idx] = ov;
     if (dd == 0) a.part_ml[((size_t)head * a.nsplit + split) * G + g] = make_float2(M, l);
   }
+  // after the streaming loop, so these stores never sit among its loads
+  if constexpr (APP) store_new_row<RB>(a, head, split, wave, lane);
 
 }
 
@@ -326,7 +363,7 @@ __device__ __forceinline__ void attend_bf16_step(const Chunk16 (&qf)[Bf16Step<D>
   }
 }
 
-template <int D, int G, bool BIAS>
+template <int D, int G, bool BIAS, bool APP>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   static_assert(G <= 8, "heads of a group live in lane rows 0 and 1");
   constexpr int NCH = Bf16Step<D>::NCH;
@@ -359,7 +396,8 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   for (int i = 0; i < 4; ++i) lpart[i] = 0.f;
 
   const int kb = split * a.chunk;
-  const int ke = min(L, kb + a.chunk);
+  // APP: the loop stops before the appended entry, which is taken below
+  const int ke = min(APP ? a.new_key : L, kb + a.chunk);
   const int stride = kWaves * KPS;
   int base = kb + wave * KPS;
   Bf16Step<D> sA, sB;
@@ -372,6 +410,12 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
     load_bf16_step<D, BIAS>(Kh, Vh, bh, base + stride, ke, col, grp, sA);
     attend_bf16_step<D, G>(qf, a.c2, base, ke, col, grp, sB, mrun, lpart, o);
     base += stride;
+  }
+  // the appended entry: one masked step of wave 0 of the workgroup that owns
+  // it, reading the caller's rows (bias 0)
+  if (APP && wave == 0 && a.new_key >= kb && a.new_key < kb + a.chunk) {
+    load_bf16_step<D, false>(a.k_new + (size_t)head * RB, a.v_new + (size_t)head * RB, nullptr, 0, 1, col, grp, sA);
+    attend_bf16_step<D, G>(qf, a.c2, 0, 1, col, grp, sA, mrun, lpart, o);
   }
 
   // l per head: sum the 16 columns of its lane row
@@ -422,6 +466,8 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
     po[idx] = ov;
     if (dd == 0) a.part_ml[((size_t)head * a.nsplit + split) * G + g] = make_float2(M, l);
   }
+  // after the streaming loop, so these stores never sit among its loads
+  if constexpr (APP) store_new_row<RB>(a, head, split, wave, lane);
 }
 
 // out[head * G + g] = sum over chunks of o * 2^(m - M) / sum of l * 2^(m - M),
@@ -496,16 +542,17 @@ __global__ __launch_bounds__(kReduceThreads) void decode_reduce_kernel(const flo
 template <typename T, int D, int G>
 hipError_t launch_g(int64_t heads, const DecodePlan& p, DecodeArgs& a, hipStream_t st) {
   const dim3 grid(p.nsplit, (unsigned)heads), blk(kThreads);
+  const bool app = a.new_key >= 0;
   if constexpr (sizeof(T) == 2) {
-    if (a.bias)
-      hipLaunchKernelGGL((decode_mfma_kernel<D, G, true>), grid, blk, 0, st, a);
-    else
-      hipLaunchKernelGGL((decode_mfma_kernel<D, G, false>), grid, blk, 0, st, a);
+    if (a.bias && app) hipLaunchKernelGGL((decode_mfma_kernel<D, G, true, true>), grid, blk, 0, st, a);
+    else if (a.bias) hipLaunchKernelGGL((decode_mfma_kernel<D, G, true, false>), grid, blk, 0, st, a);
+    else if (app) hipLaunchKernelGGL((decode_mfma_kernel<D, G, false, true>), grid, blk, 0, st, a);
+    else hipLaunchKernelGGL((decode_mfma_kernel<D, G, false, false>), grid, blk, 0, st, a);
   } else {
-    if (a.bias)
-      hipLaunchKernelGGL((decode_split_kernel<T, D, G, true>), grid, blk, 0, st, a);
-    else
-      hipLaunchKernelGGL((decode_split_kernel<T, D, G, false>), grid, blk, 0, st, a);
+    if (a.bias && app) hipLaunchKernelGGL((decode_split_kernel<T, D, G, true, true>), grid, blk, 0, st, a);
+    else if (a.bias) hipLaunchKernelGGL((decode_split_kernel<T, D, G, true, false>), grid, blk, 0, st, a);
+    else if (app) hipLaunchKernelGGL((decode_split_kernel<T, D, G, false, true>), grid, blk, 0, st, a);
+    else hipLaunchKernelGGL((decode_split_kernel<T, D, G, false, false>), grid, blk, 0, st, a);
   }
   hipLaunchKernelGGL((decode_reduce_kernel<D>), dim3((unsigned)heads, G), dim3(kReduceThreads), 0, st, a.part_o,
                      a.part_ml, a.out, p.nsplit, G);
@@ -527,30 +574,7 @@ hipError_t launch_td(int64_t heads, int G, const DecodePlan& p, DecodeArgs& a, h
   }
 }
 
-// Writes the new token's key and value rows at entry `len` of every head's
-// cache and a zero bias there (new tokens absorbed nothing: R = 1).
-__global__ __launch_bounds__(64) void decode_append_kernel(const char* k_new, const char* v_new, char* K, char* V,
-                                                           float* bias, int len, int stride, int row_bytes) {
-  const int64_t head = blockIdx.x;
-  char* kd = K + ((size_t)head * stride + len) * row_bytes;
-  char* vd = V + ((size_t)head * stride + len) * row_bytes;
-  for (int c = threadIdx.x; c * 16 < row_bytes; c += 64) {
-    store16(kd + c * 16, load16(k_new + (size_t)head * row_bytes + c * 16));
-    store16(vd + c * 16, load16(v_new + (size_t)head * row_bytes + c * 16));
-  }
-  if (bias && threadIdx.x == 0) bias[(size_t)head * stride + len] = 0.f;
-}
-
 }  // namespace
-
-hipError_t launch_decode_append(int64_t heads, int len, int stride, int d, int dtype, const void* k_new,
-                                const void* v_new, void* K, void* V, float* bias, hipStream_t st) {
-  const int row_bytes = d * (dtype == SELKV_BF16 ? 2 : 4);
-  hipLaunchKernelGGL(decode_append_kernel, dim3((unsigned)heads), dim3(64), 0, st,
-                     static_cast<const char*>(k_new), static_cast<const char*>(v_new), static_cast<char*>(K),
-                     static_cast<char*>(V), bias, len, stride, row_bytes);
-  return hipGetLastError();
-}
 
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
   DecodePlan p{};
@@ -571,9 +595,21 @@ DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
 
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int stride, int d, int G, int dtype,
                          float scale, const DecodePlan& p, const void* q, const void* K, const void* V,
-                         const float* bias, float* out, void* ws, hipStream_t st) {
+                         const float* bias, float* out, void* ws, hipStream_t st, const void* k_new,
+                         const void* v_new) {
   (void)n_heads_kv;
   DecodeArgs a{};
+  if (k_new) {   // the last entry is appended by this step
+    a.k_new = static_cast<const char*>(k_new);
+    a.v_new = static_cast<const char*>(v_new);
+    a.K_w = const_cast<char*>(static_cast<const char*>(K));
+    a.V_w = const_cast<char*>(static_cast<const char*>(V));
+    a.bias_w = const_cast<float*>(bias);
+    a.new_key = cache_len - 1;
+  } else {
+    a.k_new = a.v_new = static_cast<const char*>(K);   // never selected: no entry has key -1
+    a.new_key = -1;
+  }
   a.stride = stride;
   a.q = static_cast<const char*>(q);
   a.K = static_cast<const char*>(K);

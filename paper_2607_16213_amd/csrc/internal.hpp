@@ -98,11 +98,12 @@ hipError_t launch_union_select(const Shape& s, const UnionPlan& p, const float* 
 hipError_t launch_union_bias(const Shape& s, const float* r1, float* bias, float alpha, hipStream_t st);
 hipError_t launch_rope_reposition(const Shape& s, int dtype, const int32_t* kept, void* K_out, double theta,
                                   hipStream_t st);
-// cache_len valid entries per head, `stride` entries apart in memory (stride >= cache_len)
+// cache_len valid entries per head, `stride` entries apart in memory (stride >= cache_len).
+// With k_new / v_new the last entry (cache_len - 1) is read from them (bias 0)
+// and stored into K, V (and bias, if any) by the same launch.
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int stride, int d, int G, int dtype,
                          float scale, const DecodePlan& plan, const void* q, const void* K, const void* V,
-                         const float* bias, float* out, void* ws, hipStream_t st);
-hipError_t launch_decode_append(int64_t heads, int len, int stride, int d, int dtype, const void* k_new,
-                                const void* v_new, void* K, void* V, float* bias, hipStream_t st);
+                         const float* bias, float* out, void* ws, hipStream_t st, const void* k_new = nullptr,
+                         const void* v_new = nullptr);
 
 }  // namespace selkv

@@ -340,11 +340,9 @@ SELKV_API selkv_status selkv_decode_append(const selkv_params* p, const void* q,
   const DecodePlan plan = plan_decode(heads, cache_len + 1, p->head_dim, p->group);
   selkv_status st = check_ws(ws, ws_bytes, plan.bytes);
   if (st != SELKV_OK) return st;
-  hipError_t e = launch_decode_append(heads, cache_len, capacity, p->head_dim, p->kv_dtype, k_new, v_new, K, V,
-                                      bias, stream);
-  if (e != hipSuccess) return SELKV_EHIP;
+  // one launch: the new entry is read from k_new / v_new and stored into the cache on the way
   return hip_status(launch_decode(heads, p->n_heads_kv, cache_len + 1, capacity, p->head_dim, p->group,
-                                  p->kv_dtype, eff_scale(p), plan, q, K, V, bias, out, ws, stream));
+                                  p->kv_dtype, eff_scale(p), plan, q, K, V, bias, out, ws, stream, k_new, v_new));
 }
 
 SELKV_API const char* selkv_status_string(selkv_status s) {

@@ -737,6 +737,34 @@ def test_decode_with_appended_tokens(S, name):
     assert torch.equal(bias.cpu(), bh)
 
 
+def test_decode_append_from_empty_cache_without_bias(S):
+    """Generation from an empty cache with no bias array (fp32, d 64, G 1):
+    the first step attends over the new token alone (output = its value),
+    every later step over all tokens appended so far."""
+    p = S.params(batch=2, n_heads_kv=3, group=1, head_dim=64, seq_len=64, window=8, kv_dtype="fp32")
+    B, H, G, d = 2, 3, 1, 64
+    steps = 40
+    Kc = torch.zeros((B, H, steps, d), dtype=torch.float32, device=DEV)
+    Vc = torch.zeros_like(Kc)
+    ws = S.workspace(p, S.CALL_DECODE, DEV, steps)
+    out = torch.empty((B, H * G, d), dtype=torch.float32, device=DEV)
+    g = torch.Generator().manual_seed(5)
+    Kh, Vh = torch.zeros((B, H, steps, d)), torch.zeros((B, H, steps, d))
+    for step in range(steps):
+        q = torch.randn((B, H * G, d), generator=g)
+        kn, vn = torch.randn((B, H, d), generator=g), torch.randn((B, H, d), generator=g)
+        S.decode_append(p, q.to(DEV), kn.to(DEV), vn.to(DEV), Kc, Vc, None, step, out, ws)
+        torch.cuda.synchronize()
+        Kh[:, :, step], Vh[:, :, step] = kn, vn
+        got = out.cpu().double().numpy()
+        if step == 0:
+            np.testing.assert_allclose(got, vn.double().numpy().reshape(B, H * G, d), rtol=1e-6, atol=1e-6)
+        ref = O.decode_batched(np64(q), np64(Kh[:, :, :step + 1]), np64(Vh[:, :, :step + 1]), None, G,
+                               1.0 / math.sqrt(d))
+        assert_close_rows(got, ref, TOL["fp32"], f"append step {step}")
+    assert torch.equal(Kc.cpu(), Kh) and torch.equal(Vc.cpu(), Vh)
+
+
 # ------------------------------------------------------------------ alternative readings as modes
 READINGS = [
     # many empty buckets: bucket 4 at a 10% budget leaves most buckets without a kept token
