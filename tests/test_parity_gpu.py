@@ -218,6 +218,9 @@ EDGE = [
     dict(batch=1, H=1, G=8, d=128, n=640, W=64, dtype="bf16"),                 # 512 window rows: row groups
     dict(batch=1, H=1, G=5, d=128, n=256, W=40, dtype="fp32"),                 # fp32 row groups
     dict(batch=1, H=2, G=2, d=64, n=400, W=32, dtype="bf16", gate_threshold=0.3, gate_temperature=0.25, alpha=1.0),
+    dict(batch=1, H=2, G=2, d=64, n=128, W=16, dtype="fp32", budget_ratio=1 / 128),  # m = 1: the recent slot only
+    dict(batch=1, H=1, G=4, d=128, n=300, W=24, dtype="bf16", scale=0.05),     # explicit softmax scale
+    dict(batch=2, H=1, G=2, d=64, n=40, W=8, dtype="bf16", bucket=64),         # n shorter than one bucket
 ]
 
 
