@@ -408,44 +408,57 @@ __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
   }
 }
 
-// One wave per head: evicted tokens in ascending order, 64 at a time; each
-// token's rank among equal targets in its group of 64 comes from ballots.
-// The write cursors live in LDS; slots are swept in ranges of kCursorSlots.
-constexpr int kCursorSlots = 16384;
+// One wave per (head, range of kScatterSlots slots): it reads every evicted
+// token of the head in ascending order, 64 at a time, and places those whose
+// target lies in its range; each token's rank among equal targets in its
+// group of 64 comes from ballots, the write cursors live in LDS.  The targets
+// are loaded kScatterAhead groups ahead with clamped indices, and every lane
+// stores (lanes without a token into a sink), so no memory access sits
+// behind a branch and the wave never waits for its own stores.  A single
+// wave's LDS accesses stay in program order, so no barrier is needed between
+// reading a cursor and advancing it.
+constexpr int kScatterBits = 10;
+constexpr int kScatterSlots = 1 << kScatterBits;
+constexpr int kScatterAhead = 8;
 
 __global__ __launch_bounds__(64) void group_scatter_kernel(const int32_t* target, const int32_t* off, int32_t* list,
-                                                           int ne, int m) {
-  __shared__ int32_t cur[kCursorSlots];
-  const int64_t head = blockIdx.x;
+                                                           int32_t* sink, int ne, int m) {
+  __shared__ int32_t cur[kScatterSlots];
+  const int64_t head = blockIdx.y;
+  const int s0 = blockIdx.x * kScatterSlots;
   const int lane = threadIdx.x;
   const int32_t* th = target + (size_t)head * ne;
   const int32_t* oh = off + (size_t)head * (m + 1);
   int32_t* lh = list + (size_t)head * ne;
-  int nbits = 1;
-  while ((1 << nbits) < kCursorSlots) ++nbits;
+  const int range = min(kScatterSlots, m - s0);
+  for (int s = lane; s < range; s += 64) cur[s] = oh[s0 + s];
+  __syncthreads();
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int s0 = 0; s0 < m; s0 += kCursorSlots) {
-    const int range = min(kCursorSlots, m - s0);
-    for (int s = lane; s < range; s += 64) cur[s] = oh[s0 + s];
-    __syncthreads();
-    for (int base = 0; base < ne; base += 64) {
-      const int e = base + lane;
-      const int t = (e < ne ? th[e] : -1) - s0;       // slot relative to the range
+  const int nbatch = (ne + 63) / 64;
+  int tq[kScatterAhead];
+#pragma unroll
+  for (int k = 0; k < kScatterAhead; ++k) tq[k] = th[min(k * 64 + lane, ne - 1)];
+  for (int b0 = 0; b0 < nbatch; b0 += kScatterAhead) {
+#pragma unroll
+    for (int k = 0; k < kScatterAhead; ++k) {
+      const int e = (b0 + k) * 64 + lane;
+      const int t = (e < ne ? tq[k] : -1) - s0;            // slot relative to the range
+      tq[k] = th[min((b0 + k + kScatterAhead) * 64 + lane, ne - 1)];
       const bool valid = t >= 0 && t < range;
       uint64_t peers = __ballot(valid);
-      for (int b = 0; b < nbits; ++b) {                 // lanes with the same slot
-        const bool bit = (t >> b) & 1;
-        const uint64_t ones = __ballot(valid && bit);
-        peers &= bit ? ones : ~ones;
+#pragma unroll
+      for (int bit = 0; bit < kScatterBits; ++bit) {       // lanes with the same slot
+        const bool one = (t >> bit) & 1;
+        const uint64_t ones = __ballot(valid && one);
+        peers &= one ? ones : ~ones;
       }
       if (!valid) peers = 0ull;
       const int rank = __popcll(peers & below);
-      const int start = valid ? cur[t] : 0;
-      if (valid) lh[start + rank] = e;
+      const int start = cur[valid ? t : 0];
+      int32_t* dst = valid ? lh + start + rank : sink + lane;
+      *dst = e;
       const bool last = valid && ((peers >> lane) >> 1) == 0ull;   // highest lane of its slot
-      __syncthreads();   // every peer has read the cursor
       if (last) cur[t] = start + rank + 1;
-      __syncthreads();
     }
   }
 }
@@ -605,7 +618,8 @@ GroupPlan plan_group(const Shape& s) {
   p.off_off = 0;
   p.cursor_off = align256((size_t)s.heads * (s.m + 1) * sizeof(int32_t));
   p.list_off = p.cursor_off;
-  p.bytes = p.list_off + align256((ne > 0 ? ne : 1) * (size_t)s.heads * sizeof(int32_t));
+  p.sink_off = p.list_off + align256((ne > 0 ? ne : 1) * (size_t)s.heads * sizeof(int32_t));
+  p.bytes = p.sink_off + align256(64 * sizeof(int32_t));
   return p;
 }
 
@@ -651,7 +665,8 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
                        st, target, off, ne, s.m);
   hipLaunchKernelGGL(group_scan_kernel, dim3((unsigned)s.heads), dim3(1024), 0, st, off, s.m);
   if (ne > 0)
-    hipLaunchKernelGGL(group_scatter_kernel, dim3((unsigned)s.heads), dim3(64), 0, st, target, off, list, ne, s.m);
+    hipLaunchKernelGGL(group_scatter_kernel, dim3((s.m + kScatterSlots - 1) / kScatterSlots, (unsigned)s.heads),
+                       dim3(64), 0, st, target, off, list, reinterpret_cast<int32_t*>(w + p.sink_off), ne, s.m);
   return hipGetLastError();
 }
 

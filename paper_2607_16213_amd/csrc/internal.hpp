@@ -42,7 +42,7 @@ struct DecodePlan {
 
 // Workspace of the grouping by target slot (full-cosine routing).
 struct GroupPlan {
-  size_t off_off, cursor_off, list_off, bytes;
+  size_t off_off, cursor_off, list_off, sink_off, bytes;   // sink: stores of lanes with nothing to place
 };
 
 // Workspace of the GQA union mode: flags, mean keys and the shared set per
