@@ -410,21 +410,34 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   }
 }
 
-// Centred moving average of width K over the candidate range, zero outside.
+// Centred moving average of width K over the candidate range, zero outside:
+// each workgroup stages its kPoolOut outputs' inputs plus the
+// K - 1 halo values in LDS with coalesced loads (zeros outside [0, n_cand)),
+// then each output sums its K neighbours from LDS in ascending position.
+constexpr int kPoolOut = 1024;
+constexpr int kPoolMaxK = 1025;
+
 __global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* cbuf, float* score, int n, int n_cand,
                                                              int K) {
+  __shared__ float tile[kPoolOut + kPoolMaxK - 1];
   const int64_t head = blockIdx.y;
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= n_cand) return;
-  const float* c = cbuf + (size_t)head * n;
+  const int j0 = blockIdx.x * kPoolOut;
   const int h = K / 2;
-  float s = 0.f;
-  for (int t = -h; t <= h; ++t) {
-    const int jj = j + t;
+  const float* c = cbuf + (size_t)head * n;
+  for (int i = threadIdx.x; i < kPoolOut + 2 * h; i += kThreads) {
+    const int jj = j0 - h + i;
     const float v = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
-    s += (jj >= 0 && jj < n_cand) ? v : 0.f;
+    tile[i] = (jj >= 0 && jj < n_cand) ? v : 0.f;
   }
-  score[(size_t)head * n_cand + j] = s / (float)K;
+  __syncthreads();
+  for (int q = threadIdx.x; q < kPoolOut; q += kThreads) {
+    const int j = j0 + q;
+    if (j < n_cand) {
+      float sum = 0.f;
+      for (int t = 0; t < K; ++t) sum += tile[q + t];
+      score[(size_t)head * n_cand + j] = sum / (float)K;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -755,7 +768,7 @@ hipError_t launch_t(const Shape& s, const ScorePlan& p, ScoreArgs& a, float* sco
   hipLaunchKernelGGL(score_combine_kernel, dim3((unsigned)s.heads), blk, 0, st, a);
   hipLaunchKernelGGL((score_colsum_kernel<T, D, NRB, RW>), dim3(p.nchunks, (unsigned)s.heads), blk, 0, st, a);
   if (s.n_cand > 0)
-    hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kThreads - 1) / kThreads, (unsigned)s.heads), blk, 0,
+    hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kPoolOut - 1) / kPoolOut, (unsigned)s.heads), blk, 0,
                        st, a.cbuf, score, s.n, s.n_cand, pool_kernel);
   return hipGetLastError();
 }
@@ -781,7 +794,7 @@ hipError_t launch_tiled(const Shape& s, const ScorePlan& p, ScoreArgs& a, float*
   hipLaunchKernelGGL(score_combine_kernel, dim3((unsigned)s.heads), blk, 0, st, a);
   hipLaunchKernelGGL(score_colsum_tiled<D>, dim3(p.nchunks2, (unsigned)s.heads), blk, 0, st, a);
   if (s.n_cand > 0)
-    hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kThreads - 1) / kThreads, (unsigned)s.heads), blk, 0,
+    hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kPoolOut - 1) / kPoolOut, (unsigned)s.heads), blk, 0,
                        st, a.cbuf, score, s.n, s.n_cand, pool_kernel);
   return hipGetLastError();
 }

@@ -20,6 +20,7 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
   if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
   if (p->window < 1 || p->window > p->seq_len) return SELKV_EINVAL;
   if (p->pool_kernel < 1 || (p->pool_kernel % 2) == 0) return SELKV_EINVAL;
+  if (p->pool_kernel > 1025) return SELKV_EUNSUPPORTED;
   if (p->recent < 0) return SELKV_EINVAL;
   if (p->bucket < 1) return SELKV_EINVAL;
   if (p->bucket > 64) return SELKV_EUNSUPPORTED;

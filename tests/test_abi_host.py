@@ -92,6 +92,7 @@ def test_validation_codes(S):
     assert st(S.params(seq_len=100, kv_dtype=7)) == 2           # EDTYPE
     assert st(S.params(seq_len=100, window=101)) == 1           # W > n
     assert st(S.params(seq_len=100, pool_kernel=4)) == 1        # even K
+    assert st(S.params(seq_len=100, pool_kernel=1027)) == 3     # K above 1025: unsupported
     assert st(S.params(seq_len=100, budget_ratio=0.0)) == 1
     assert st(S.params(seq_len=100, budget_ratio=1.5)) == 1
     assert st(S.params(seq_len=3, window=3, budget_ratio=0.25)) == 1   # m = 0
