@@ -89,17 +89,23 @@ __global__ __launch_bounds__(kThreads) void coattn_route_kernel(CoArgs a) {
   const char* Qh = a.Q + (size_t)head * a.R * RB;
   const int R = a.R, nrb = (R + 15) / 16;
   const int win0 = n - a.W;
+  // query rows and row statistics of the next 16-row block load while the
+  // current block is used (indices clamped; rows past R are masked by off)
   Chunk16 qf[NCH];
+  float offn[4];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) qf[c] = load16(Qh + (size_t)min(col, R - 1) * RB + (c * 4 + grp) * 16);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) offn[i] = st[min(grp * 4 + i, R - 1)].x;
   for (int rb = 0; rb < nrb; ++rb) {
     float off[4];
     int rpos[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = rb * 16 + grp * 4 + i;
-      off[i] = r < R ? st[r].x : kNegInf;
+      off[i] = r < R ? offn[i] : kNegInf;
       rpos[i] = win0 + (r < R ? r % a.W : 0);
+      offn[i] = st[min(r + 16, R - 1)].x;
     }
     // logits of the block's 16 rows against the bucket's keys
     f32x4 x[NT];
