@@ -157,6 +157,15 @@ def _dev(t: torch.Tensor, shape, dtype, name):
     return t
 
 
+def _nbytes(ws):
+    """Size in bytes of a workspace tensor (any dtype), 0 for none."""
+    if ws is None:
+        return 0
+    if not ws.is_cuda or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    return ws.numel() * ws.element_size()
+
+
 def _kvdt(p: Params):
     return torch.bfloat16 if p.kv_dtype == BF16 else torch.float32
 
@@ -170,7 +179,7 @@ def score(p, K, V, Qwin, score_out, attn, vnorm, ws, stream=None):
     _dev(score_out, (B, H, n - mr), torch.float32, "score")
     _dev(attn, (B, H, n), torch.float32, "attn"); _dev(vnorm, (B, H, n), torch.float32, "vnorm")
     _check(lib.selkv_score(ctypes.byref(p), _ptr(K), _ptr(V), _ptr(Qwin), _ptr(score_out), _ptr(attn), _ptr(vnorm),
-                           _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)), "selkv_score")
+                           _ptr(ws), _nbytes(ws), _stream(stream)), "selkv_score")
 
 
 def select(p, score_in, kept, evicted, ws=None, stream=None):
@@ -180,7 +189,7 @@ def select(p, score_in, kept, evicted, ws=None, stream=None):
     _dev(kept, (B, H, m), torch.int32, "kept_idx")
     _dev(evicted, (B, H, n - m), torch.int32, "evicted_idx")
     _check(lib.selkv_select(ctypes.byref(p), _ptr(score_in), _ptr(kept), _ptr(evicted), _ptr(ws),
-                            ws.numel() if ws is not None else 0, _stream(stream)), "selkv_select")
+                            _nbytes(ws), _stream(stream)), "selkv_select")
 
 
 def route_coattn(p, K, Qwin, kept, evicted, target, ws, stream=None):
@@ -192,7 +201,7 @@ def route_coattn(p, K, Qwin, kept, evicted, target, ws, stream=None):
     _dev(kept, (B, H, m), torch.int32, "kept_idx"); _dev(evicted, (B, H, n - m), torch.int32, "evicted_idx")
     _dev(target, (B, H, n - m), torch.int32, "target")
     _check(lib.selkv_route_coattn(ctypes.byref(p), _ptr(K), _ptr(Qwin), _ptr(kept), _ptr(evicted), _ptr(target),
-                                  _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
+                                  _ptr(ws), _nbytes(ws), _stream(stream)),
            "selkv_route_coattn")
 
 
@@ -207,7 +216,7 @@ def merge(p, K, V, attn, vnorm, kept, evicted, K_out, V_out, target, gate, ws, s
     _dev(target, (B, H, n - m), torch.int32, "target"); _dev(gate, (B, H, n - m), torch.float32, "gate")
     _check(lib.selkv_merge(ctypes.byref(p), _ptr(K), _ptr(V), _ptr(attn), _ptr(vnorm), _ptr(kept), _ptr(evicted),
                            _ptr(K_out), _ptr(V_out), _ptr(target), _ptr(gate), _ptr(ws),
-                           ws.numel() if ws is not None else 0, _stream(stream)), "selkv_merge")
+                           _nbytes(ws), _stream(stream)), "selkv_merge")
 
 
 def bias(p, attn, kept, evicted, target, gate, bias_out, ws, stream=None):
@@ -218,7 +227,7 @@ def bias(p, attn, kept, evicted, target, gate, bias_out, ws, stream=None):
     _dev(target, (B, H, n - m), torch.int32, "target"); _dev(gate, (B, H, n - m), torch.float32, "gate")
     _dev(bias_out, (B, H, m), torch.float32, "bias")
     _check(lib.selkv_bias(ctypes.byref(p), _ptr(attn), _ptr(kept), _ptr(evicted), _ptr(target), _ptr(gate),
-                          _ptr(bias_out), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
+                          _ptr(bias_out), _ptr(ws), _nbytes(ws), _stream(stream)),
            "selkv_bias")
 
 
@@ -241,7 +250,7 @@ def decode_attn(p, q, K, V, bias_in, out, ws, stream=None):
         _dev(bias_in, (B, H, L), torch.float32, "bias")
     _dev(out, (B, H * p.group, d), torch.float32, "out")
     _check(lib.selkv_decode_attn(ctypes.byref(p), _ptr(q), _ptr(K), _ptr(V), _ptr(bias_in), L, _ptr(out), _ptr(ws),
-                                 ws.numel() if ws is not None else 0, _stream(stream)), "selkv_decode_attn")
+                                 _nbytes(ws), _stream(stream)), "selkv_decode_attn")
 
 
 def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=None):
@@ -258,7 +267,7 @@ def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=
     _dev(out, (B, H * p.group, d), torch.float32, "out")
     _check(lib.selkv_decode_append(ctypes.byref(p), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(K), _ptr(V),
                                    _ptr(bias_io), int(cache_len), cap, _ptr(out), _ptr(ws),
-                                   ws.numel() if ws is not None else 0, _stream(stream)), "selkv_decode_append")
+                                   _nbytes(ws), _stream(stream)), "selkv_decode_append")
 
 
 class Compressor:
