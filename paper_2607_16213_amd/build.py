@@ -1,4 +1,5 @@
-"""Builds libselkv.so (HIP, gfx950) in-tree from csrc/*.hip with hipcc.
+"""Builds libselkv.so (HIP, gfx950) in-tree from csrc/*.hip with hipcc, and
+the plain-C ABI consumer examples/selkv_c_demo with gcc against it.
 
     python -m paper_2607_16213_amd.build          # or build.build()
 """
@@ -17,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libselkv.so")
+DEMO_SRC = os.path.join(PKG, "examples", "selkv_c_demo.c")
+DEMO = os.path.join(PKG, "examples", "selkv_c_demo")
 ARCH = "gfx950"
 
 COMMON_FLAGS = [
@@ -66,7 +69,23 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
     os.replace(tmp, LIB)
+    build_demo()
     return LIB
+
+
+def build_demo() -> str:
+    """Compile the C consumer with gcc: C11, the public header only, linked
+    against the in-tree libselkv.so (found at run time through its rpath)."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           f"-I{INCLUDE}", f"-I{rocm}/include", DEMO_SRC, "-o", DEMO + ".tmp",
+           f"-L{PKG}", "-lselkv", f"-L{rocm}/lib", "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/..", f"-Wl,-rpath,{rocm}/lib"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"gcc failed on {DEMO_SRC}:\n{r.stdout}{r.stderr}")
+    os.replace(DEMO + ".tmp", DEMO)
+    return DEMO
 
 
 if __name__ == "__main__":
