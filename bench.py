@@ -26,6 +26,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+# the compression calls of one step: score, select, and the fused merge + bias (steps 3 - 6)
+STAGES = ("score", "select", "merge_bias")
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
 METRIC = "SelKV compress tokens/s @32k,100k; biased-decode step µs; % HBM/MFMA peak"
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_ctx100k_pmc.txt")
@@ -125,11 +127,10 @@ class Job:
         if ev: ev[1].record()
         s.select(p, c.score, c.kept, c.evicted)
         if ev: ev[2].record()
-        s.merge(p, self.Kf, self.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
-                c.ws_merge)
+        # steps 3 - 6: routing, gate, merge and the ratio bias in one pass
+        s.merge_bias(p, self.Kf, self.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
+                     c.bias, c.ws_merge)
         if ev: ev[3].record()
-        s.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, c.ws_bias)
-        if ev: ev[4].record()
 
     def _decode_eager(self, steps):
         c, B = self.comp, self.w.batch
@@ -190,10 +191,10 @@ def stage_bytes(w, m):
     score = heads * (2 * n * d * e + G * W * d * e + 4 * (n - mr) + 8 * n)
     select = heads * (4 * (n - mr) + 4 * n)
     merge = heads * (n * d * e + m * d * e + 8 * n + 4 * n + 2 * m * d * e + 8 * ev)
-    bias = heads * (4 * m + 4 * ev + 4 * ev + 8 * ev + 4 * m)
+    merge_bias = merge + heads * 4 * m          # the fused call also writes the bias
     per_decode = B * H * (2 * m * d * e + 4 * m) + B * H * G * d * (e + 4)
     full_decode = B * H * (2 * n * d * e) + B * H * G * d * (e + 4)
-    return dict(score=score, select=select, merge=merge, bias=bias), per_decode, full_decode
+    return dict(score=score, select=select, merge_bias=merge_bias), per_decode, full_decode
 
 
 def cpu_baseline(job, n_heads, dev):
@@ -243,18 +244,18 @@ def measure(job, steps, warmup):
         job.compress()
         job.decode()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     t0 = time.perf_counter()
     for s in range(steps):
         ev = evs[s]
         job.compress(ev)
         job.decode()
-        ev[5].record()
+        ev[4].record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
-    st = {k: 0.0 for k in ("score", "select", "merge", "bias", "decode")}
+    st = {k: 0.0 for k in STAGES + ("decode",)}
     for ev in evs:
-        for i, k in enumerate(("score", "select", "merge", "bias", "decode")):
+        for i, k in enumerate(STAGES + ("decode",)):
             st[k] += ev[i].elapsed_time(ev[i + 1]) / steps      # ms
     return wall, st
 
@@ -269,11 +270,10 @@ def measure_variant(job, note, reps=3, **modes):
                      window=w.window, kv_dtype=w.dtype, budget_ratio=w.budgets[0], **modes)
     c, dev = job.comp, job.K.device
     ws_sel = selkv.workspace(p, selkv.CALL_SELECT, dev)
-    ws_merge = selkv.workspace(p, selkv.CALL_MERGE, dev)
-    ws_bias = selkv.workspace(p, selkv.CALL_BIAS, dev)
+    ws_merge = selkv.workspace(p, selkv.CALL_MERGE_BIAS, dev)
     coattn = p.route_mode == selkv.ROUTE_COATTN
     ws_route = selkv.workspace(p, selkv.CALL_ROUTE, dev) if coattn else None
-    names = ("score", "select") + (("route",) if coattn else ()) + ("merge", "bias")
+    names = ("score", "select") + (("route",) if coattn else ()) + ("merge_bias",)
 
     def run(ev=None):
         i = 0
@@ -288,11 +288,8 @@ def measure_variant(job, note, reps=3, **modes):
             selkv.route_coattn(p, job.Kf, job.Qf, c.kept, c.evicted, c.target, ws_route)
             i += 1
             if ev: ev[i].record()
-        selkv.merge(p, job.Kf, job.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target, c.gate,
-                    ws_merge)
-        i += 1
-        if ev: ev[i].record()
-        selkv.bias(p, c.attn, c.kept, c.evicted, c.target, c.gate, c.bias, ws_bias)
+        selkv.merge_bias(p, job.Kf, job.Vf, c.attn, c.vnorm, c.kept, c.evicted, c.K_out, c.V_out, c.target,
+                         c.gate, c.bias, ws_merge)
         i += 1
         if ev: ev[i].record()
 
@@ -465,14 +462,14 @@ def main():
         job.build_graph()
     wall, st = measure(job, args.steps, args.warmup)
     sb, per_decode, full_decode_bytes = stage_bytes(w, job.m)
-    comp_ms = st["score"] + st["select"] + st["merge"] + st["bias"]
+    comp_ms = sum(st[k] for k in STAGES)
     value = w.seq_len * w.batch / (comp_ms / 1e3)
     n_dec = T * w.layers
     dec_us = st["decode"] * 1e3 / n_dec
     decode_gbs = per_decode / (dec_us * 1e-6) / 1e9
 
     stages = {}
-    for k in ("score", "select", "merge", "bias"):
+    for k in STAGES:
         gbs = sb[k] / (st[k] * 1e-3) / 1e9
         stages[k] = {"ms": round(st[k], 4), "alg_bytes": sb[k], "achieved_GBs": round(gbs, 1),
                      "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
@@ -537,14 +534,14 @@ def main():
             j32.compress()
             j32.build_graph()
         _, st32 = measure(j32, max(1, args.steps), 1)
-        c32 = st32["score"] + st32["select"] + st32["merge"] + st32["bias"]
+        c32 = sum(st32[k] for k in STAGES)
         sb32, pd32, _ = stage_bytes(w32, j32.m)
         d32 = st32["decode"] * 1e3 / (j32.T * w32.layers)
         out["ctx32k"] = {"compress_tokens_per_s": round(w32.seq_len / (c32 / 1e3), 1), "compress_ms": round(c32, 4),
                          "decode_us_per_layer_step": round(d32, 3),
                          "decode_GBs": round(pd32 / (d32 * 1e-6) / 1e9, 1),
                          "score_GBs": round(sb32["score"] / (st32["score"] * 1e-3) / 1e9, 1),
-                         "merge_GBs": round(sb32["merge"] / (st32["merge"] * 1e-3) / 1e9, 1)}
+                         "merge_bias_GBs": round(sb32["merge_bias"] / (st32["merge_bias"] * 1e-3) / 1e9, 1)}
         del j32
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(job, args.cpu_heads, dev)

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define SELKV_ABI_VERSION 4
+#define SELKV_ABI_VERSION 5
 
 typedef enum selkv_status {
   SELKV_OK = 0,
@@ -104,7 +104,8 @@ typedef enum selkv_call {
   SELKV_CALL_MERGE = 2,
   SELKV_CALL_BIAS = 3,
   SELKV_CALL_DECODE = 4,
-  SELKV_CALL_ROUTE = 5      /* selkv_route_coattn */
+  SELKV_CALL_ROUTE = 5,     /* selkv_route_coattn */
+  SELKV_CALL_MERGE_BIAS = 6 /* selkv_merge_bias */
 } selkv_call;
 
 /* Problem description, named as in the paper.  Fill it with
@@ -270,6 +271,26 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
 SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,
                                   const int32_t* evicted_idx, const int32_t* target, const float* gate,
                                   float* bias, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Steps 3 to 6 of Algorithm 1 in one call: selkv_merge and selkv_bias
+ * (Sec. 3.4 - 3.6, Eq. 3 - 6) with the same params, fused.
+ *
+ * The merge pass already forms, for every kept slot, the absorbed mass
+ * sum_{j->s} g_j a_j that Eq. 5 divides by; it writes bias[s] = alpha * ln R_s
+ * from that same sum, so attn, target and gate are not read back and the
+ * bias pass over the evicted tokens disappears.  Outputs are bit for bit
+ * those of selkv_merge followed by selkv_bias (both sum a slot's weights in
+ * one fixed order).  Under UNION selection the per-head R - 1 go to the
+ * workspace and one more small pass averages them over the heads of each
+ * cache, as selkv_bias does.
+ * In:  as selkv_merge (under COATTN routing, target from selkv_route_coattn).
+ * Out: K_out, V_out, target, gate as selkv_merge; bias [B, H_kv, m] fp32 as
+ *      selkv_bias.
+ * Workspace: selkv_workspace_size(p, SELKV_CALL_MERGE_BIAS, 0). */
+SELKV_API selkv_status selkv_merge_bias(const selkv_params* p, const void* K, const void* V, const float* attn,
+                                        const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx,
+                                        void* K_out, void* V_out, int32_t* target, float* gate, float* bias,
+                                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Step 7 of Algorithm 1: RoPE repositioning (Sec. 3.6 last subsection,
  * Eq. 7; the paper leaves it off for long contexts).

@@ -142,6 +142,11 @@ struct RawSlice {
   }
 };
 
+// A value every lane of the wave holds alike, moved to a scalar register.
+__device__ __forceinline__ float uniform(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
 __device__ __forceinline__ float xor_shfl(float v, int mask) { return __shfl_xor(v, mask, 64); }
 __device__ __forceinline__ int xor_shfl(int v, int mask) { return __shfl_xor(v, mask, 64); }
 
@@ -159,6 +164,39 @@ __device__ __forceinline__ float sum16(float v) {
   v += row_ror<2>(v);
   v += row_ror<1>(v);
   return v;
+}
+
+// A merge weight g * a rounded on its own: the product is never fused into
+// the sum it feeds, so the merge and the bias kernels add the same values.
+__device__ __forceinline__ float weight_rn(float g, float a) {
+#pragma clang fp contract(off)
+  return g * a;
+}
+
+// Absorbed-mass sums in the merge kernels' order.  A kept slot's weights
+// g * a (Eq. 5) are accumulated by lane group: group q (lanes 16q .. 16q+15)
+// adds entries q, q + 4, q + 8, ... of the slot's segment in turn, and the
+// four group sums combine as (s0 + s1) + (s2 + s3).  The bias kernels form
+// the same sums from a one-entry-per-lane layout with the two helpers below,
+// so the R of Eq. 6 they compute is bit for bit the one the merge divides by.
+// seg_sum_add: adds a 64-entry chunk of the segment (lane i holds entry i of
+// the chunk, 0 past the segment's end; chunks start at multiples of 64 from
+// the segment start) to the running group sum s, which lane l holds for
+// group l & 3.  seg_sum_total: the combined sum, on every lane.
+__device__ __forceinline__ float seg_sum_add(float s, float c, int lane) {
+#pragma unroll
+  for (int t = 0; t < 16; ++t) s += __shfl(c, 4 * t + (lane & 3), 64);
+  return s;
+}
+
+__device__ __forceinline__ float seg_sum_total(float s) {
+  return (__shfl(s, 0, 64) + __shfl(s, 1, 64)) + (__shfl(s, 2, 64) + __shfl(s, 3, 64));
+}
+
+// alpha * ln R with R = 1 + absorbed / a (Eq. 6), exactly 0 when nothing was
+// absorbed; raw: R - 1 itself, which the union mode averages over heads first.
+__device__ __forceinline__ float ratio_bias(float absorbed, float a, float alpha, bool raw) {
+  return absorbed > 0.f ? (raw ? absorbed / a : alpha * log1pf(absorbed / a)) : 0.f;
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

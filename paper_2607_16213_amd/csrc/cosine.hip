@@ -517,14 +517,11 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     if (li < l1) {
       const int e = lh[li];
       jp = eh[e];
-      w = gh[e] * ah[jp];
+      w = weight_rn(gh[e], ah[jp]);
     }
     const int cnt = min(64, l1 - lb);
     if (!VALUES) {
-      float t = w;
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) t += xor_shfl(t, o);
-      wsum += t;
+      wsum = seg_sum_add(wsum, w, lane);   // the running group sums, in the values pass's order
       continue;
     }
     constexpr int kBatch = 4;
@@ -563,8 +560,8 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     }
   }
   if (!VALUES) {
-    if (lane == 0)
-      a.bias[(size_t)head * m + s] = wsum > 0.f ? (a.raw ? wsum / a_s : a.alpha * log1pf(wsum / a_s)) : 0.f;
+    wsum = seg_sum_total(wsum);
+    if (lane == 0) a.bias[(size_t)head * m + s] = ratio_bias(wsum, a_s, a.alpha, a.raw != 0);
     return;
   }
 #pragma unroll
@@ -581,6 +578,8 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
   }
   wsum += xor_shfl(wsum, 16);
   wsum += xor_shfl(wsum, 32);
+  // fused call: the Eq. 6 bias of the slot from the same absorbed mass
+  if (a.bias != nullptr && lane == 0) a.bias[(size_t)head * m + s] = ratio_bias(wsum, a_s, a.alpha, a.raw != 0);
   if (grp == 0) {
     const char* krow = a.K + ((size_t)head * n + pos) * RB;
     const char* vrow = a.V + ((size_t)head * n + pos) * RB;
@@ -692,7 +691,7 @@ hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, con
   a.alpha = alpha;
   a.raw = raw ? 1 : 0;
   const dim3 grid((s.m + kWaves - 1) / kWaves, (unsigned)s.heads);
-  const bool values = bias == nullptr;
+  const bool values = V_out != nullptr;   // else the bias pass alone
 #define SELKV_GM(T, D)                                                                                     \
   do {                                                                                                     \
     if (values && merge_keys)                                                                              \

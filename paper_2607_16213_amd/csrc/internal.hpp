@@ -68,13 +68,14 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
                                const void* K, const void* V, const float* attn, const float* vnorm,
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
                                void* V_out, int32_t* target, float* gate, bool merge_keys, bool nearest,
-                               hipStream_t st);
+                               float* bias, float alpha, bool raw, hipStream_t st);
+// bias (nullable): the fused Eq. 6 output per kept slot, alpha * ln R or (raw) R - 1
 // targets given (co-attention routing): per bucket, grouped by target slot
 hipError_t launch_merge_targets(const Shape& s, int dtype, int bucket, int gate_mode, float tau, float temp,
                                 const void* K, const void* V, const float* attn, const float* vnorm,
                                 const int32_t* kept, const int32_t* evicted, const int32_t* offs,
                                 const int32_t* target, void* K_out, void* V_out, float* gate, bool merge_keys,
-                                hipStream_t st);
+                                float* bias, float alpha, bool raw, hipStream_t st);
 // score pass 1 and its combine only: the row statistics at plan.stats_off of ws
 hipError_t launch_row_stats(const Shape& s, const ScorePlan& p, int dtype, float scale, const void* K,
                             const void* Qwin, void* ws, hipStream_t st);
@@ -89,6 +90,7 @@ hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float t
                                const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
                                float* gate, hipStream_t st);
 hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st);
+// values pass when V_out is set (bias, when also set, from the same sums); bias pass alone otherwise
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
                               const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,

@@ -74,8 +74,11 @@ struct MergeArgs {
   char* V_out;
   int32_t* target;
   float* gate;
+  float* bias;      // fused Eq. 6 output per kept slot, or null
   int n, m, nb, B, gate_mode;
   float tau, inv_temp;
+  float alpha;
+  int raw;          // bias holds R - 1 (union mode) instead of alpha * ln R
 };
 
 // Nearest-kept fallback: the evicted tokens of the empty buckets between two
@@ -165,7 +168,7 @@ __device__ __forceinline__ void absorb_run(const MergeArgs& a, const char* Kh, c
           g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
         }
         if (i < cnt) {
-          const float w = g * ajv[u];
+          const float w = weight_rn(g, ajv[u]);
 #pragma unroll
           for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
           if constexpr (MK) {
@@ -309,7 +312,7 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
         }
       }
       if (valid) {
-        const float w = g * ajv[u];
+        const float w = weight_rn(g, ajv[u]);
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
         if constexpr (MK) {
@@ -365,6 +368,27 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
     wf += xor_shfl(wf, 32);
     wl += xor_shfl(wl, 16);
     wl += xor_shfl(wl, 32);
+  }
+
+  // the fused Eq. 6 bias: only the target slot (and, with the fallback, the
+  // bucket's outer slots) absorbed anything, so the ratios are formed once
+  // per wave, from the same sums the merged rows divide by; one coalesced
+  // store of the bucket's nk <= 64 biases, ahead of the row loop
+  if (a.bias != nullptr) {
+    auto slot_w = [&](int k) {
+      if constexpr (NR) return (k == tslot ? wsum : 0.f) + (k == k0 ? wf : 0.f) + (k == k1 - 1 ? wl : 0.f);
+      else return k == tslot ? wsum : 0.f;
+    };
+    const bool raw = a.raw != 0;
+    const float b_t = ratio_bias(slot_w(tslot), a_t, a.alpha, raw);
+    float b_0 = 0.f, b_1 = 0.f;
+    if constexpr (NR) {
+      b_0 = ratio_bias(slot_w(k0), __shfl(a_k, 0, 64), a.alpha, raw);
+      b_1 = ratio_bias(slot_w(k1 - 1), __shfl(a_k, nk - 1, 64), a.alpha, raw);
+    }
+    const int k = k0 + lane;
+    if (lane < nk)
+      a.bias[(size_t)head * m + k] = k == tslot ? b_t : (NR && k == k0) ? b_0 : (NR && k == k1 - 1) ? b_1 : 0.f;
   }
 
   // write the bucket's kept rows: keys gathered (or merged), values copied or merged;
@@ -562,7 +586,7 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
           g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
         }
         if (i < s1) {
-          const float w = g * ajv[u];
+          const float w = weight_rn(g, ajv[u]);
 #pragma unroll
           for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vr[u].get(e), acc[e]);
           if constexpr (MK) {
@@ -600,6 +624,7 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
         kr.store(Ko + (size_t)k * RB, col);
         vr.store(Vo + (size_t)k * RB, col);
       }
+      if (a.bias != nullptr && col == 0) a.bias[(size_t)head * m + k] = ratio_bias(wsum, a_t, a.alpha, a.raw != 0);
     }
     written |= 1ull << ki;
   }
@@ -619,6 +644,7 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
       if (i < nk && !((written >> i) & 1ull)) {
         kr[u].store(Ko + (size_t)(k0 + i) * RB, col);
         vr[u].store(Vo + (size_t)(k0 + i) * RB, col);
+        if (a.bias != nullptr && col == 0) a.bias[(size_t)head * m + k0 + i] = 0.f;
       }
     }
   }
@@ -636,6 +662,35 @@ struct BiasArgs {
   float alpha;
   int raw;   // write absorbed / a (R - 1) instead of alpha * ln R
 };
+
+// Sum of g * a over a bucket's evicted entries routed to slot k (lane e holds
+// entry e: its target t_e and contribution c_e, 0 past ne), in the order in
+// which the merge kernels accumulate a slot's weights: one segment when, as
+// bucket routing guarantees, every routed token of the bucket shares a
+// target; otherwise the entries routed to k in ascending evicted order (the
+// segment order of the given-targets merge).
+__device__ __forceinline__ float bucket_mass(int t_e, float c_e, int k, int ne, int lane) {
+  const int t0 = __shfl(t_e, 0, 64);
+  if (__ballot(lane >= ne || t_e == t0) == ~0ull) {
+    const float tot = seg_sum_total(seg_sum_add(0.f, c_e, lane));
+    return k == t0 ? tot : 0.f;
+  }
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  int r = 0;   // entries of k's segment so far
+  for (int i = 0; i < ne; ++i) {
+    const int t = __shfl(t_e, i, 64);
+    const float c = __shfl(c_e, i, 64);
+    if (t == k) {
+      const int q = r & 3;
+      if (q == 0) s0 += c;
+      else if (q == 1) s1 += c;
+      else if (q == 2) s2 += c;
+      else s3 += c;
+      ++r;
+    }
+  }
+  return (s0 + s1) + (s2 + s3);
+}
 
 // One wave per kBiasBuckets consecutive buckets.  For each bucket lane e
 // loads the e-th evicted entry and its contribution g * a, lane i the i-th
@@ -689,33 +744,15 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
   float c_e[kBiasBuckets], a_k[kBiasBuckets];
 #pragma unroll
   for (int bi = 0; bi < kBiasBuckets; ++bi) {
-    c_e[bi] = g_e[bi] * ah[j_e[bi]];
+    c_e[bi] = weight_rn(g_e[bi], ah[j_e[bi]]);
     a_k[bi] = ah[pos_k[bi]];
   }
 #pragma unroll
   for (int bi = 0; bi < kBiasBuckets; ++bi) {
     if (!ok[bi]) continue;                       // wave-uniform
     const int k = k0[bi] + lane;
-    float absorbed = 0.f;
-    // bucket routing sends every routed token of a bucket to one slot: then
-    // one wave sum does; otherwise add per slot in ascending evicted order
-    const int t0 = __shfl(t_e[bi], 0, 64);
-    const bool same = __ballot(lane >= ne[bi] || t_e[bi] == t0) == ~0ull;
-    if (same) {
-      float tot = c_e[bi];
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
-      absorbed = (k == t0) ? tot : 0.f;
-    } else {
-      for (int i = 0; i < ne[bi]; ++i) {
-        const int t = __shfl(t_e[bi], i, 64);
-        const float c = __shfl(c_e[bi], i, 64);
-        if (t == k) absorbed += c;
-      }
-    }
-    if (k < k1[bi])
-      a.bias[(size_t)head * m + k] =
-          absorbed > 0.f ? (a.raw ? absorbed / a_k[bi] : a.alpha * log1pf(absorbed / a_k[bi])) : 0.f;
+    const float absorbed = bucket_mass(t_e[bi], c_e[bi], k, ne[bi], lane);
+    if (k < k1[bi]) a.bias[(size_t)head * m + k] = ratio_bias(absorbed, a_k[bi], a.alpha, a.raw != 0);
   }
 }
 
@@ -723,14 +760,13 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
 // target is `slot`; the wave total, in a fixed order.
 __device__ __forceinline__ float run_mass(const BiasArgs& a, const int32_t* th, const float* gh, const float* ah,
                                           int ea, int eb, int shift, int slot, int lane) {
-  float tot = 0.f;
+  float s = 0.f;
   for (int c0 = ea; c0 < eb; c0 += 64) {
     const int e = c0 + lane;
-    if (e < eb && th[e] == slot) tot += gh[e] * ah[e + shift];
+    const float c = (e < eb && th[e] == slot) ? weight_rn(gh[e], ah[e + shift]) : 0.f;
+    s = seg_sum_add(s, c, lane);
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
-  return tot;
+  return seg_sum_total(s);
 }
 
 // Nearest-kept fallback: one wave per non-empty bucket adds to its kept
@@ -754,33 +790,17 @@ __global__ __launch_bounds__(kThreads) void bias_nearest_kernel(BiasArgs a) {
   if (k0 >= k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // empty bucket or inconsistent list
   const int nk = k1 - k0, ne = e1 - e0;
   const int t_e = lane < ne ? th[e0 + lane] : -1;
-  const float c_e = lane < ne ? gh[e0 + lane] * ah[eh[e0 + lane]] : 0.f;
+  const float c_e = lane < ne ? weight_rn(gh[e0 + lane], ah[eh[e0 + lane]]) : 0.f;
   const float a_k = lane < nk ? ah[kh[k0 + lane]] : 1.f;
   const int k = k0 + lane;
-  float absorbed = 0.f;
-  // the routing sends the bucket's own tokens to one slot: one wave sum;
-  // otherwise per slot in ascending evicted order
-  const int t0 = __shfl(t_e, 0, 64);
-  if (__ballot(lane >= ne || t_e == t0) == ~0ull) {
-    float tot = c_e;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) tot += xor_shfl(tot, off);
-    absorbed = (k == t0) ? tot : 0.f;
-  } else {
-    for (int i = 0; i < ne; ++i) {
-      const int t = __shfl(t_e, i, 64);
-      const float c = __shfl(c_e, i, 64);
-      if (t == k) absorbed += c;
-    }
-  }
+  // the merge's order: the bucket's own tokens, then the left run, then the right run
+  float absorbed = bucket_mass(t_e, c_e, k, ne, lane);
   const GapRuns r = gap_runs(kh, n, m, a.B, start, end, k0, k1);
   const float left = run_mass(a, th, gh, ah, r.eL0, r.eL1, k0, k0, lane);
   const float right = run_mass(a, th, gh, ah, r.eR0, r.eR1, k1, k1 - 1, lane);
   if (k == k0) absorbed += left;
   if (k == k1 - 1) absorbed += right;
-  if (lane < nk)
-    a.bias[(size_t)head * m + k] =
-        absorbed > 0.f ? (a.raw ? absorbed / a_k : a.alpha * log1pf(absorbed / a_k)) : 0.f;
+  if (lane < nk) a.bias[(size_t)head * m + k] = ratio_bias(absorbed, a_k, a.alpha, a.raw != 0);
 }
 
 }  // namespace
@@ -799,7 +819,7 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
                                const void* K, const void* V, const float* attn, const float* vnorm,
                                const int32_t* kept, const int32_t* evicted, const int32_t* offs, void* K_out,
                                void* V_out, int32_t* target, float* gate, bool merge_keys, bool nearest,
-                               hipStream_t st) {
+                               float* bias, float alpha, bool raw, hipStream_t st) {
   MergeArgs a{};
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);
@@ -812,6 +832,9 @@ hipError_t launch_merge_bucket(const Shape& s, int dtype, int bucket, int gate_m
   a.V_out = static_cast<char*>(V_out);
   a.target = target;
   a.gate = gate;
+  a.bias = bias;
+  a.alpha = alpha;
+  a.raw = raw ? 1 : 0;
   a.n = s.n;
   a.m = s.m;
   a.nb = s.nb;
@@ -845,7 +868,7 @@ hipError_t launch_merge_targets(const Shape& s, int dtype, int bucket, int gate_
                                 const void* K, const void* V, const float* attn, const float* vnorm,
                                 const int32_t* kept, const int32_t* evicted, const int32_t* offs,
                                 const int32_t* target, void* K_out, void* V_out, float* gate, bool merge_keys,
-                                hipStream_t st) {
+                                float* bias, float alpha, bool raw, hipStream_t st) {
   MergeArgs a{};
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);
@@ -858,6 +881,9 @@ hipError_t launch_merge_targets(const Shape& s, int dtype, int bucket, int gate_
   a.V_out = static_cast<char*>(V_out);
   a.target = const_cast<int32_t*>(target);   // read only by this kernel
   a.gate = gate;
+  a.bias = bias;
+  a.alpha = alpha;
+  a.raw = raw ? 1 : 0;
   a.n = s.n;
   a.m = s.m;
   a.nb = s.nb;

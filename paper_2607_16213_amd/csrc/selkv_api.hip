@@ -79,11 +79,67 @@ size_t route_bytes(const selkv_params* p, const Shape& s) {
 // bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
 size_t bias_base_bytes(const selkv_params* p, const Shape& s) { return merge_bytes(p, s); }
 
+// bias workspace: the routing's own scratch, then (union mode) the per-head R - 1
+size_t bias_bytes(const selkv_params* p, const Shape& s) {
+  const size_t base = bias_base_bytes(p, s);
+  return is_union(p) ? round256(base) + plan_union(s).ratio_bytes : base;
+}
+
 selkv_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return SELKV_OK;
   if (!ws || ws_bytes < need) return SELKV_EWORKSPACE;
   if (!aligned(ws, 256)) return SELKV_EALIGN;
   return SELKV_OK;
+}
+
+selkv_status check_merge_args(const Shape& s, const void* K, const void* V, const float* attn, const float* vnorm,
+                              const int32_t* kept_idx, const int32_t* evicted_idx, void* K_out, void* V_out,
+                              int32_t* target, float* gate) {
+  const bool has_ev = s.n > s.m;
+  if (!K || !V || !attn || !vnorm || !kept_idx || !K_out || !V_out) return SELKV_EINVAL;
+  if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(K_out, 16) || !aligned(V_out, 16) || !aligned(attn, 4) ||
+      !aligned(vnorm, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
+      !aligned(gate, 4))
+    return SELKV_EALIGN;
+  return SELKV_OK;
+}
+
+// Steps 3 - 5 (and, when bias is set, the fused step 6) on validated arguments.
+selkv_status run_merge(const selkv_params* p, const Shape& s, const void* K, const void* V, const float* attn,
+                       const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx, void* K_out,
+                       void* V_out, int32_t* target, float* gate, float* bias, bool raw, void* ws,
+                       hipStream_t stream) {
+  const bool mk = p->merge_keys != 0;
+  hipError_t e;
+  if (p->route_mode == SELKV_ROUTE_COATTN) {
+    // targets given by selkv_route_coattn: grouped by target inside each bucket
+    int32_t* offs = static_cast<int32_t*>(ws);
+    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    return hip_status(launch_merge_targets(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
+                                           p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs,
+                                           target, K_out, V_out, gate, mk, bias, p->alpha, raw, stream));
+  }
+  if (p->route_mode != SELKV_ROUTE_FULL_COSINE) {
+    // bucket routings: one wave per bucket (plus its runs of empty buckets under the nearest-kept fallback)
+    int32_t* offs = static_cast<int32_t*>(ws);
+    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
+    if (e != hipSuccess) return SELKV_EHIP;
+    return hip_status(launch_merge_bucket(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
+                                          p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs, K_out,
+                                          V_out, target, gate, mk, p->route_mode == SELKV_ROUTE_BUCKET_NEAREST, bias,
+                                          p->alpha, raw, stream));
+  }
+  // all-pairs routing: match, group by target slot, merge per slot
+  e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm, kept_idx,
+                          evicted_idx, target, gate, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  const GroupPlan gp = plan_group(s);
+  e = launch_group(s, gp, target, ws, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
+  return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out, V_out,
+                                       bias, p->alpha, raw, mk, stream));
 }
 
 }  // namespace
@@ -142,9 +198,7 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
     case SELKV_CALL_MERGE: *bytes = merge_bytes(p, s); return SELKV_OK;
     case SELKV_CALL_ROUTE: *bytes = route_bytes(p, s); return SELKV_OK;
     case SELKV_CALL_BIAS:
-      *bytes = bias_base_bytes(p, s);
-      if (is_union(p)) *bytes = round256(*bytes) + plan_union(s).ratio_bytes;
-      return SELKV_OK;
+    case SELKV_CALL_MERGE_BIAS: *bytes = bias_bytes(p, s); return SELKV_OK;
     default: return SELKV_EINVAL;
   }
 }
@@ -212,44 +266,32 @@ SELKV_API selkv_status selkv_merge(const selkv_params* p, const void* K, const v
   Shape s;
   selkv_status st = make_shape(p, &s);
   if (st != SELKV_OK) return st;
-  const bool has_ev = s.n > s.m;
-  if (!K || !V || !attn || !vnorm || !kept_idx || !K_out || !V_out) return SELKV_EINVAL;
-  if (has_ev && (!evicted_idx || !target || !gate)) return SELKV_EINVAL;
-  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(K_out, 16) || !aligned(V_out, 16) || !aligned(attn, 4) ||
-      !aligned(vnorm, 4) || !aligned(kept_idx, 4) || !aligned(evicted_idx, 4) || !aligned(target, 4) ||
-      !aligned(gate, 4))
-    return SELKV_EALIGN;
+  if ((st = check_merge_args(s, K, V, attn, vnorm, kept_idx, evicted_idx, K_out, V_out, target, gate)) != SELKV_OK)
+    return st;
   if ((st = check_ws(ws, ws_bytes, merge_bytes(p, s))) != SELKV_OK) return st;
-  const bool mk = p->merge_keys != 0;
-  hipError_t e;
-  if (p->route_mode == SELKV_ROUTE_COATTN) {
-    // targets given by selkv_route_coattn: grouped by target inside each bucket
-    int32_t* offs = static_cast<int32_t*>(ws);
-    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
-    if (e != hipSuccess) return SELKV_EHIP;
-    return hip_status(launch_merge_targets(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
-                                           p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs,
-                                           target, K_out, V_out, gate, mk, stream));
-  }
-  if (p->route_mode != SELKV_ROUTE_FULL_COSINE) {
-    // bucket routings: one wave per bucket (plus its runs of empty buckets under the nearest-kept fallback)
-    int32_t* offs = static_cast<int32_t*>(ws);
-    e = launch_bucket_offsets(s, p->bucket, kept_idx, offs, stream);
-    if (e != hipSuccess) return SELKV_EHIP;
-    return hip_status(launch_merge_bucket(s, p->kv_dtype, p->bucket, p->gate_mode, p->gate_threshold,
-                                          p->gate_temperature, K, V, attn, vnorm, kept_idx, evicted_idx, offs, K_out,
-                                          V_out, target, gate, mk, p->route_mode == SELKV_ROUTE_BUCKET_NEAREST,
-                                          stream));
-  }
-  // all-pairs routing: match, group by target slot, merge per slot
-  e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm, kept_idx,
-                          evicted_idx, target, gate, stream);
-  if (e != hipSuccess) return SELKV_EHIP;
-  const GroupPlan gp = plan_group(s);
-  e = launch_group(s, gp, target, ws, stream);
-  if (e != hipSuccess) return SELKV_EHIP;
-  return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out, V_out,
-                                       nullptr, 0.f, false, mk, stream));
+  return run_merge(p, s, K, V, attn, vnorm, kept_idx, evicted_idx, K_out, V_out, target, gate, nullptr, false, ws,
+                   stream);
+}
+
+SELKV_API selkv_status selkv_merge_bias(const selkv_params* p, const void* K, const void* V, const float* attn,
+                                        const float* vnorm, const int32_t* kept_idx, const int32_t* evicted_idx,
+                                        void* K_out, void* V_out, int32_t* target, float* gate, float* bias,
+                                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape s;
+  selkv_status st = make_shape(p, &s);
+  if (st != SELKV_OK) return st;
+  if ((st = check_merge_args(s, K, V, attn, vnorm, kept_idx, evicted_idx, K_out, V_out, target, gate)) != SELKV_OK)
+    return st;
+  if (!bias) return SELKV_EINVAL;
+  if (!aligned(bias, 4)) return SELKV_EALIGN;
+  const bool uni = is_union(p);
+  if ((st = check_ws(ws, ws_bytes, bias_bytes(p, s))) != SELKV_OK) return st;
+  // union mode: the merge writes each head's R - 1 into the workspace
+  float* dst = uni ? reinterpret_cast<float*>(static_cast<char*>(ws) + round256(merge_bytes(p, s))) : bias;
+  if ((st = run_merge(p, s, K, V, attn, vnorm, kept_idx, evicted_idx, K_out, V_out, target, gate, dst, uni, ws,
+                      stream)) != SELKV_OK || !uni)
+    return st;
+  return hip_status(launch_union_bias(s, dst, bias, p->alpha, stream));
 }
 
 SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, const int32_t* kept_idx,
@@ -268,8 +310,7 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
   // workspace and one more pass averages it over the heads of each cache
   const bool uni = is_union(p);
   const size_t base = bias_base_bytes(p, s);
-  const size_t need = uni ? round256(base) + plan_union(s).ratio_bytes : base;
-  if ((st = check_ws(ws, ws_bytes, need)) != SELKV_OK) return st;
+  if ((st = check_ws(ws, ws_bytes, bias_bytes(p, s))) != SELKV_OK) return st;
   float* dst = uni ? reinterpret_cast<float*>(static_cast<char*>(ws) + round256(base)) : bias;
   hipError_t e;
   if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {

@@ -20,8 +20,8 @@ F32, BF16 = 0, 1
 GATE_COSINE, GATE_DROP, GATE_MERGE_ALL = 0, 1, 2
 ROUTE_BUCKET, ROUTE_FULL_COSINE, ROUTE_BUCKET_NEAREST, ROUTE_COATTN = 0, 1, 2, 3
 SELECT_PER_HEAD, SELECT_UNION = 0, 1
-ABI_VERSION = 4
-CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE, CALL_ROUTE = range(6)
+ABI_VERSION = 5
+CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE, CALL_ROUTE, CALL_MERGE_BIAS = range(7)
 STATUS = {0: "SELKV_OK", 1: "SELKV_EINVAL", 2: "SELKV_EDTYPE", 3: "SELKV_EUNSUPPORTED", 4: "SELKV_EALIGN",
           5: "SELKV_EWORKSPACE", 6: "SELKV_EHIP"}
 GATE_MODES = {"cosine": GATE_COSINE, "drop": GATE_DROP, "merge_all": GATE_MERGE_ALL}
@@ -76,6 +76,7 @@ def _load():
         "selkv_route_coattn": (ctypes.c_int, [P, vp, vp, ip, ip, ip, vp, sz, vp]),
         "selkv_merge": (ctypes.c_int, [P, vp, vp, fp, fp, ip, ip, vp, vp, ip, fp, vp, sz, vp]),
         "selkv_bias": (ctypes.c_int, [P, fp, ip, ip, ip, fp, fp, vp, sz, vp]),
+        "selkv_merge_bias": (ctypes.c_int, [P, vp, vp, fp, fp, ip, ip, vp, vp, ip, fp, fp, vp, sz, vp]),
         "selkv_decode_attn": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp, sz, vp]),
         "selkv_rope_reposition": (ctypes.c_int, [P, ip, vp, ctypes.c_double, vp]),
         "selkv_decode_append": (ctypes.c_int, [P, vp, vp, vp, vp, vp, fp, i32, i32, fp, vp, sz, vp]),
@@ -219,6 +220,22 @@ def merge(p, K, V, attn, vnorm, kept, evicted, K_out, V_out, target, gate, ws, s
                            _nbytes(ws), _stream(stream)), "selkv_merge")
 
 
+def merge_bias(p, K, V, attn, vnorm, kept, evicted, K_out, V_out, target, gate, bias_out, ws, stream=None):
+    """selkv_merge and selkv_bias in one pass (the bias from the merge's own sums)."""
+    B, H, n, d = p.batch, p.n_heads_kv, p.seq_len, p.head_dim
+    m, mr, ms = budget(p)
+    dt = _kvdt(p)
+    _dev(K, (B, H, n, d), dt, "K"); _dev(V, (B, H, n, d), dt, "V")
+    _dev(attn, (B, H, n), torch.float32, "attn"); _dev(vnorm, (B, H, n), torch.float32, "vnorm")
+    _dev(kept, (B, H, m), torch.int32, "kept_idx"); _dev(evicted, (B, H, n - m), torch.int32, "evicted_idx")
+    _dev(K_out, (B, H, m, d), dt, "K_out"); _dev(V_out, (B, H, m, d), dt, "V_out")
+    _dev(target, (B, H, n - m), torch.int32, "target"); _dev(gate, (B, H, n - m), torch.float32, "gate")
+    _dev(bias_out, (B, H, m), torch.float32, "bias")
+    _check(lib.selkv_merge_bias(ctypes.byref(p), _ptr(K), _ptr(V), _ptr(attn), _ptr(vnorm), _ptr(kept),
+                                _ptr(evicted), _ptr(K_out), _ptr(V_out), _ptr(target), _ptr(gate), _ptr(bias_out),
+                                _ptr(ws), _nbytes(ws), _stream(stream)), "selkv_merge_bias")
+
+
 def bias(p, attn, kept, evicted, target, gate, bias_out, ws, stream=None):
     B, H, n = p.batch, p.n_heads_kv, p.seq_len
     m, mr, ms = budget(p)
@@ -272,8 +289,9 @@ def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=
 
 class Compressor:
     """Owns the output and scratch tensors of one problem size and runs the
-    compression calls (score, select, [route_coattn,] merge, bias) on the current
-    stream.  Allocation happens once, in the constructor."""
+    compression calls (score, select, [route_coattn,] merge_bias, or merge then
+    bias with fused=False) on the current stream.  Allocation happens once, in
+    the constructor."""
 
     def __init__(self, p: Params, device):
         self.p = p
@@ -294,19 +312,22 @@ class Compressor:
         self.bias = torch.empty((B, H, m), dtype=f32, device=device)
         self.ws_score = workspace(p, CALL_SCORE, device)
         self.ws_select = workspace(p, CALL_SELECT, device)
-        self.ws_merge = workspace(p, CALL_MERGE, device)
-        self.ws_bias = workspace(p, CALL_BIAS, device)
+        self.ws_merge = workspace(p, CALL_MERGE_BIAS, device)   # covers merge and bias alone too
         self.ws_route = workspace(p, CALL_ROUTE, device) if p.route_mode == ROUTE_COATTN else None
 
-    def run(self, K, V, Qwin, stream=None):
+    def run(self, K, V, Qwin, stream=None, fused=True):
         p = self.p
         score(p, K, V, Qwin, self.score, self.attn, self.vnorm, self.ws_score, stream)
         select(p, self.score, self.kept, self.evicted, self.ws_select, stream)
         if p.route_mode == ROUTE_COATTN:
             route_coattn(p, K, Qwin, self.kept, self.evicted, self.target, self.ws_route, stream)
-        merge(p, K, V, self.attn, self.vnorm, self.kept, self.evicted, self.K_out, self.V_out, self.target,
-              self.gate, self.ws_merge, stream)
-        bias(p, self.attn, self.kept, self.evicted, self.target, self.gate, self.bias, self.ws_bias, stream)
+        if fused:
+            merge_bias(p, K, V, self.attn, self.vnorm, self.kept, self.evicted, self.K_out, self.V_out, self.target,
+                       self.gate, self.bias, self.ws_merge, stream)
+        else:
+            merge(p, K, V, self.attn, self.vnorm, self.kept, self.evicted, self.K_out, self.V_out, self.target,
+                  self.gate, self.ws_merge, stream)
+            bias(p, self.attn, self.kept, self.evicted, self.target, self.gate, self.bias, self.ws_merge, stream)
         return self
 
     def outputs(self):

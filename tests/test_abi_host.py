@@ -63,7 +63,7 @@ def test_params_init_defaults(S):
     assert p.struct_size == ctypes.sizeof(S.Params)
     assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
     assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
-    assert S.lib.selkv_abi_version() == 4
+    assert S.lib.selkv_abi_version() == 5
     assert S.lib.selkv_status_string(0) == b"success"
 
 
@@ -189,7 +189,7 @@ def test_coattn_route_validation_and_workspace(S):
     b = ctypes.c_size_t()
     bad = S.params(seq_len=256, route_mode=4)
     assert S.lib.selkv_workspace_size(ctypes.byref(bad), S.CALL_ROUTE, 0, ctypes.byref(b)) == 1
-    assert S.lib.selkv_workspace_size(ctypes.byref(p), 6, 0, ctypes.byref(b)) == 1
+    assert S.lib.selkv_workspace_size(ctypes.byref(p), 7, 0, ctypes.byref(b)) == 1
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
@@ -201,3 +201,30 @@ def test_coattn_route_call_validation(S):
     assert f(ctypes.byref(p), fake, fake, fake, None, fake, fake, 1 << 30, None) == 1        # evicted needed
     assert f(ctypes.byref(p), fake, mis, fake, fake, fake, fake, 1 << 30, None) == 4         # Qwin 16-byte aligned
     assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 64, None) == 5             # workspace too small
+
+
+def test_merge_bias_workspace_is_the_bias_workspace(S):
+    """The fused merge + bias call needs the merge's routing scratch plus, in
+    union mode, the per-head ratios: exactly what selkv_bias needs."""
+    for kw in ({}, dict(route_mode="full_cosine"), dict(route_mode="bucket_nearest"), dict(route_mode="coattn"),
+               dict(select_mode="union"), dict(select_mode="union", route_mode="full_cosine")):
+        p = S.params(seq_len=1000, **kw)
+        assert S.workspace_bytes(p, S.CALL_MERGE_BIAS) == S.workspace_bytes(p, S.CALL_BIAS)
+        assert S.workspace_bytes(p, S.CALL_MERGE_BIAS) >= S.workspace_bytes(p, S.CALL_MERGE)
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_merge_bias_call_validation(S):
+    p = S.params(seq_len=256)
+    fake, mis4, mis2 = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10004), ctypes.c_void_p(0x10002)
+    f = S.lib.selkv_merge_bias
+    big = 1 << 30
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, None, fake, big, None) == 1
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, mis2, fake, big, None) == 4
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, mis4, fake, fake, fake, fake, fake, big, None) == 4
+    assert f(ctypes.byref(p), None, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, None) == 1
+    assert f(ctypes.byref(p), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, 16, None) == 5
+    union = S.params(seq_len=256, select_mode="union")
+    need = S.workspace_bytes(union, S.CALL_MERGE_BIAS)
+    assert f(ctypes.byref(union), fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, need - 1,
+             None) == 5

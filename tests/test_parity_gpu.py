@@ -127,7 +127,7 @@ def run_stagewise(S, p, K, V, Qwin, heads=None):
     for (b, h), ch in chains.items():
         t_in[b, h] = torch.as_tensor(ch["target"], dtype=torch.int32)
         g_in[b, h] = torch.as_tensor(ch["g32"], dtype=torch.float32)
-    S.bias(p, a_in, kept_in, ev_in, t_in, g_in, comp.bias, comp.ws_bias)
+    S.bias(p, a_in, kept_in, ev_in, t_in, g_in, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     alpha = float(np.float32(p.alpha))
     for (b, h), ch in chains.items():
@@ -497,7 +497,7 @@ def test_full_cosine_routing_stagewise(S, case):
         comp.gate[b, h] = torch.as_tensor(g32, dtype=torch.float32)
         chains[(b, h)]["fc_bias"] = O.ratio_bias(ch["a32"], ch["kept"], ch["ev"], target, g32,
                                                  float(np.float32(p.alpha)))
-    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     for (b, h), ch in chains.items():
         err = np.abs(np64(comp.bias[b, h]) - ch["fc_bias"]).max(initial=0)
@@ -600,7 +600,7 @@ def test_gqa_union_select_merge_bias(S, case):
                 _, v_out, _ = O.merge(K64[b, h], V64[b, h], hd["a32"], kept, ev, t_in[b, h].cpu().numpy(),
                                       g_in[b, h].cpu().double().numpy())
                 assert_close_rows(np64(comp.V_out[b, h]), v_out, tol, f"V_out[{b},{h}]")
-    S.bias(p, a_in, comp.kept, comp.evicted, t_in, g_in, comp.bias, comp.ws_bias)
+    S.bias(p, a_in, comp.kept, comp.evicted, t_in, g_in, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     for b in range(B):
         for h in range(H):
@@ -851,7 +851,7 @@ def test_alternative_readings_stagewise(S, case):
             assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(r["kept"])]), f"K_out[{b},{h}]"
         comp.target[b, h] = torch.as_tensor(r["target"], dtype=torch.int32)
         comp.gate[b, h] = torch.as_tensor(r["g32"], dtype=torch.float32)
-    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     for (b, h), r in refs.items():
         err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
@@ -976,7 +976,7 @@ def test_coattn_routing_stagewise(S, case):
         sel = torch.as_tensor(untouched, dtype=torch.long)
         assert torch.equal(comp.V_out[b, h].cpu()[sel], V[b, h].cpu()[torch.as_tensor(ch["kept"][untouched])])
         comp.gate[b, h] = torch.as_tensor(r["g32"], dtype=torch.float32)
-    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_bias)
+    S.bias(p, a_in, comp.kept, comp.evicted, comp.target, comp.gate, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     for (b, h), r in refs.items():
         err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
@@ -1011,3 +1011,66 @@ def test_coattn_end_to_end_llama_layer(S):
             ok = tc[b, h] >= 0
             assert (kept[b, h][tc[b, h][ok]] // Bk == ev[b, h][ok] // Bk).all()
     assert (tc != te).any(), "co-attention should route some token differently from Eq. 3"
+
+
+# ------------------------------------------------------------------ fused merge + bias (steps 3 - 6 in one pass)
+FUSED = [
+    dict(batch=1, H=2, G=4, d=128, n=2000, W=32, dtype="bf16"),
+    dict(batch=2, H=2, G=2, d=64, n=777, W=16, dtype="fp32", gate_mode=2),
+    dict(batch=1, H=2, G=2, d=128, n=640, W=16, dtype="bf16", route_mode="bucket_nearest", bucket=4,
+         budget_ratio=0.1),
+    dict(batch=1, H=2, G=2, d=64, n=513, W=16, dtype="fp32", route_mode="bucket_nearest", bucket=2,
+         budget_ratio=0.02, merge_keys=1),
+    dict(batch=1, H=2, G=4, d=128, n=1000, W=32, dtype="bf16", merge_keys=1),
+    dict(batch=1, H=2, G=4, d=128, n=1500, W=32, dtype="bf16", route_mode="coattn"),
+    dict(batch=1, H=2, G=2, d=64, n=700, W=16, dtype="fp32", route_mode="coattn", bucket=64),
+    dict(batch=1, H=2, G=4, d=128, n=1200, W=32, dtype="bf16", route_mode="full_cosine"),
+    dict(batch=2, H=4, G=2, d=128, n=900, W=32, dtype="bf16", select_mode="union"),
+    dict(batch=1, H=4, G=2, d=64, n=600, W=16, dtype="fp32", select_mode="union", route_mode="full_cosine"),
+    dict(batch=1, H=2, G=2, d=64, n=100, W=8, dtype="fp32", budget_ratio=1.0),         # nothing evicted
+]
+
+
+@pytest.mark.parametrize("case", FUSED, ids=[f"fused{i}" for i in range(len(FUSED))])
+def test_merge_bias_fused_equals_merge_then_bias(S, case):
+    """selkv_merge_bias gives bit for bit what selkv_merge followed by
+    selkv_bias gives, in every routing, gate, key and selection mode: the
+    bias kernels sum a slot's absorbed mass in the merge kernels' order."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 7 + 5, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=6, device=DEV)
+    p = make_params(S, case, **kw)
+    print(f"fused case {case} {kw}", flush=True)
+    comp = S.Compressor(p, DEV)
+    comp.run(t["K"], t["V"], t["Qwin"], fused=False)
+    torch.cuda.synchronize()
+    sep = {k: v.clone() for k, v in comp.outputs().items()}
+    for v in (comp.K_out, comp.V_out, comp.gate, comp.bias):
+        v.fill_(float("nan"))
+    comp.target.fill_(-7)
+    comp.run(t["K"], t["V"], t["Qwin"], fused=True)
+    torch.cuda.synchronize()
+    fused = comp.outputs()
+    for k in ("kept", "evicted", "target", "gate", "K_out", "V_out", "bias"):
+        a, b = sep[k], fused[k]
+        assert torch.equal(a.view(torch.int32) if a.is_floating_point() and a.element_size() == 4 else a,
+                           b.view(torch.int32) if b.is_floating_point() and b.element_size() == 4 else b), k
+    # and the bias is the oracle's for every head whose kept set and targets match it
+    K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
+    if kw.get("select_mode") == "union" or kw.get("route_mode") in ("coattn", "full_cosine"):
+        return   # covered against the oracle by their own stage-wise tests
+    alpha = float(np.float32(p.alpha))
+    for b in range(case["batch"]):
+        for h in range(case["H"]):
+            ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * case["G"]:(h + 1) * case["G"]],
+                                 window=case["W"], budget_ratio=p.budget_ratio, bucket=p.bucket,
+                                 gate_mode=GATE[p.gate_mode],
+                                 route_mode="bucket_nearest" if p.route_mode == S.ROUTE_BUCKET_NEAREST else "bucket")
+            if not np.array_equal(fused["kept"][b, h].cpu().numpy(), ch["kept"]):
+                continue
+            if not np.array_equal(fused["target"][b, h].cpu().numpy(), ch["target"]):
+                continue
+            got = np64(fused["bias"][b, h])
+            assert np.abs(got - ch["bias"]).max() <= abs(alpha) * TOL[case["dtype"]], (b, h)
