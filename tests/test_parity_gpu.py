@@ -1074,3 +1074,50 @@ def test_merge_bias_fused_equals_merge_then_bias(S, case):
                 continue
             got = np64(fused["bias"][b, h])
             assert np.abs(got - ch["bias"]).max() <= abs(alpha) * TOL[case["dtype"]], (b, h)
+
+
+# ------------------------------------------------------------------ selection: the threshold's top-12-bit bin
+def _select_case(rng, kind):
+    """(n, m, scores [2, n - 16] fp32) for a selection whose threshold falls in
+    a top-12-bit bin of a chosen population (values in [1, 1.1) share sign,
+    exponent and the top three mantissa bits)."""
+    if kind in ("at_cap", "over_cap"):
+        inbin = 12288 if kind == "at_cap" else 12289
+        hi = 7712
+        n_cand = inbin + hi
+        s = np.concatenate([1.0 + 0.1 * rng.random((2, inbin)), 4.0 + rng.random((2, hi))], axis=1)
+        s = np.stack([rng.permutation(r) for r in s])
+        ms = hi + 5000
+    elif kind == "all_equal":
+        n_cand, ms = 30000, 7000
+        s = np.full((2, n_cand), 0.75)
+    else:   # five distinct values in one (staged) bin, many exact ties at the threshold
+        n_cand, ms = 10000, 4000
+        vals = np.float32(1.0) + np.float32(2.0 ** -20) * np.arange(5, dtype=np.float32)
+        s = vals[rng.integers(0, 5, (2, n_cand))]
+    n = n_cand + 16
+    return n, ms + 16, s.astype(np.float32)
+
+
+@pytest.mark.parametrize("kind", ["at_cap", "over_cap", "all_equal", "ties"])
+def test_select_threshold_bin_staged_or_not(S, kind):
+    """The m_s-th largest score is found from a 12-bit histogram, then in LDS
+    when its bin holds at most 12288 keys and with two more passes over the
+    scores otherwise; either way the kept and evicted lists are the oracle's
+    bit for bit (equal scores: the lower position wins)."""
+    rng = np.random.default_rng({"at_cap": 1, "over_cap": 2, "all_equal": 3, "ties": 4}[kind])
+    n, m, s = _select_case(rng, kind)
+    p = S.params(batch=1, n_heads_kv=2, group=1, head_dim=64, seq_len=n, window=8, kv_dtype="fp32",
+                 budget_ratio=(m + 0.5) / n)
+    mm, mr, ms = S.budget(p)
+    assert (mm, mr) == (m, 16)
+    print(f"select {kind}: n={n} m={m}", flush=True)
+    score = torch.as_tensor(s)[None].to(DEV).contiguous()
+    kept = torch.empty((1, 2, m), dtype=torch.int32, device=DEV)
+    ev = torch.empty((1, 2, n - m), dtype=torch.int32, device=DEV)
+    S.select(p, score, kept, ev)
+    torch.cuda.synchronize()
+    for h in range(2):
+        k_ref, e_ref = O.select(s[h].astype(np.float64), n, m, mr)
+        assert np.array_equal(kept[0, h].cpu().numpy(), k_ref), (kind, h)
+        assert np.array_equal(ev[0, h].cpu().numpy(), e_ref), (kind, h)
