@@ -382,6 +382,35 @@ def measure_generation(job, steps=64, reps=3):
             "note": "append + biased decode per layer (bias 0 on appended tokens), caches m..m+steps-1 entries"}
 
 
+def measure_batched_decode(job, reps=20):
+    """One selkv_decode_attn call over all layers' compressed caches at once
+    (the leading batch is layers x sequences): the same kernels with 32x the
+    work per launch, as when many sequences decode together.  Shows the split
+    kernel's streaming rate once launch ramp and tail are amortised."""
+    torch, selkv, w = job.torch, job.selkv, job.w
+    c = job.comp
+    L, B, H, G, d = w.layers, w.batch, w.n_heads_kv, w.group, w.head_dim
+    p = selkv.params(batch=L * B, n_heads_kv=H, group=G, head_dim=d, kv_dtype=w.dtype)
+    dec = selkv.Decoder(p, job.m, job.K.device)
+    out = job.outs.view(L * B, H * G, d)
+    q = [job.Qd[t].reshape(L * B, H * G, d) for t in range(min(reps, job.T))]
+    dec.run(q[0], c.K_out, c.V_out, c.bias, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for r in range(reps):
+        dec.run(q[r % len(q)], c.K_out, c.V_out, c.bias, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    e = c.K_out.element_size()
+    nbytes = L * B * H * (2 * job.m * d * e + 4 * job.m) + L * B * H * G * d * (e + 4)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"caches_per_call": L * B, "us_per_call": round(us, 2), "alg_bytes_per_call": nbytes,
+            "achieved_GBs": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+            "note": "all layers' caches in one decode call (batch = layers x sequences)"}
+
+
 def measure_rope(job, theta=500000.0, reps=3):
     """RoPE repositioning (Eq. 7) of the whole model's compressed keys, in
     place on the job's K_out (run after the decode measurements).  Moves
@@ -502,6 +531,7 @@ def main():
         out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
         out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
 
+    out["batched_decode"] = measure_batched_decode(job)
     if not args.no_generation:
         out["generation_loop"] = measure_generation(job)
     if args.full_cosine_layers > 0:
