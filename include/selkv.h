@@ -116,7 +116,7 @@ typedef struct selkv_params {
   int32_t n_heads_kv;        /* H_kv */
   int32_t group;             /* G: query heads per KV head; H_q = G * H_kv; query head h reads KV head h / G */
   int32_t head_dim;          /* d: 64 or 128 */
-  int32_t seq_len;           /* n: prompt length (tokens in the uncompressed cache) */
+  int32_t seq_len;           /* n: prompt length (tokens in the uncompressed cache), at most 2^28 */
   int32_t window;            /* W: observation window, 1 <= W <= n (Sec. 3.2, default 32) */
   int32_t pool_kernel;       /* K: odd smoothing kernel (Sec. 3.2, default 5; at most 1025) */
   int32_t recent;            /* m_r: recent tokens always kept (Sec. 3.1, default 16) */

@@ -1,4 +1,4 @@
-// selkv_merge (BUCKET routing) and selkv_bias: Sec. 3.4 - 3.6, Eq. 3 - 6.
+// selkv_merge, selkv_bias and selkv_merge_bias under the bucket routings: Sec. 3.4 - 3.6, Eq. 3 - 6.
 //
 // Under bucket routing every evicted token and its target share one
 // positional bucket of B <= 64 tokens, so one wave owns one bucket and the
@@ -10,10 +10,14 @@
 //            write the merged target value, copy the other kept values and
 //            gather every kept key
 //   bias     per bucket: R = 1 + (sum over routed tokens of g*a) / a_i,
-//            bias = alpha * ln R (exactly 0 when nothing was absorbed)
+//            bias = alpha * ln R (exactly 0 when nothing was absorbed); the
+//            sums are taken in the merge's order, and the fused call
+//            (selkv_merge_bias) has the merge wave write them directly
 // Options: keys merged with the value weights (merge_keys), and the
 // nearest-kept fallback, under which the waves of the non-empty buckets also
 // absorb the runs of empty buckets beside them (still local, still ordered).
+// The given-targets merge (co-attention routing) groups each bucket's
+// entries by target slot instead of routing them itself.
 // Row layout of one wave: lane group g = lane / 16 takes one token (row) and
 // each of its 16 lanes one contiguous slice of d/16 elements, so a wave
 // instruction moves four consecutive rows.
@@ -80,6 +84,27 @@ struct MergeArgs {
   float alpha;
   int raw;          // bias holds R - 1 (union mode) instead of alpha * ln R
 };
+
+// base[i] = v through a 32-bit byte offset from a wave-uniform base, which
+// lets the store take its base from scalar registers (one offset VGPR
+// instead of a 64-bit address pair).  Valid while i * 4 < 2^32: per-head
+// arrays here hold at most seq_len < 2^28 entries.
+template <typename T>
+__device__ __forceinline__ void store_u32off(T* base, uint32_t i, T v) {
+  *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + i * (uint32_t)sizeof(T)) = v;
+}
+
+// Eq. 4 gate of a token whose value has dot product `dot` with its target's
+// value: clamp((cos - tau) / T, 0, 1), the cosine 0 when a norm is 0; 0
+// under DROP, 1 under MERGE_ALL.  The norm product is divided through the
+// hardware reciprocal (within 2 ulp of the quotient), which keeps the IEEE
+// division's temporaries out of the merge loops.
+__device__ __forceinline__ float gate_of(const MergeArgs& a, float dot, float vn_j, float vn_t) {
+  if (a.gate_mode == SELKV_GATE_MERGE_ALL) return 1.f;
+  if (a.gate_mode != SELKV_GATE_COSINE) return 0.f;
+  const float sim = (vn_j > 0.f && vn_t > 0.f) ? dot * __builtin_amdgcn_rcpf(vn_j * vn_t) : 0.f;
+  return fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
+}
 
 // Nearest-kept fallback: the evicted tokens of the empty buckets between two
 // non-empty ones all lie between the last kept token P before them and the
@@ -160,13 +185,7 @@ __device__ __forceinline__ void absorb_run(const MergeArgs& a, const char* Kh, c
 #pragma unroll
         for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
         dot = sum16(dot);
-        float g = 0.f;
-        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
-          g = 1.f;
-        } else if (a.gate_mode == SELKV_GATE_COSINE) {
-          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
-          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
-        }
+        const float g = gate_of(a, dot, vnjv[u], vn_t);
         if (i < cnt) {
           const float w = weight_rn(g, ajv[u]);
 #pragma unroll
@@ -177,8 +196,8 @@ __device__ __forceinline__ void absorb_run(const MergeArgs& a, const char* Kh, c
           }
           wsum += w;
           if (col == 0) {
-            th[c0 + i] = slot;
-            gh[c0 + i] = g;
+            store_u32off(th, (uint32_t)(c0 + i), slot);
+            store_u32off(gh, (uint32_t)(c0 + i), g);
           }
         }
       }
@@ -302,15 +321,7 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
 #pragma unroll
       for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
       dot = sum16(dot);
-      float g = 0.f;
-      if (tslot >= 0) {
-        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
-          g = 1.f;
-        } else if (a.gate_mode == SELKV_GATE_COSINE) {
-          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
-          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
-        }
-      }
+      const float g = tslot >= 0 ? gate_of(a, dot, vnjv[u], vn_t) : 0.f;
       if (valid) {
         const float w = weight_rn(g, ajv[u]);
 #pragma unroll
@@ -321,8 +332,8 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
         }
         wsum += w;
         if (col == 0) {
-          th[e0 + i] = tslot;
-          gh[e0 + i] = g;
+          store_u32off(th, (uint32_t)(e0 + i), tslot);
+          store_u32off(gh, (uint32_t)(e0 + i), g);
         }
       }
     }
@@ -578,13 +589,7 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
 #pragma unroll
         for (int e = 0; e < E; ++e) dot = fmaf(vr[u].get(e), vt[e], dot);
         dot = sum16(dot);
-        float g = 0.f;
-        if (a.gate_mode == SELKV_GATE_MERGE_ALL) {
-          g = 1.f;
-        } else if (a.gate_mode == SELKV_GATE_COSINE) {
-          const float sim = (vnjv[u] > 0.f && vn_t > 0.f) ? dot / (vnjv[u] * vn_t) : 0.f;
-          g = fminf(1.f, fmaxf(0.f, (sim - a.tau) * a.inv_temp));
-        }
+        const float g = gate_of(a, dot, vnjv[u], vn_t);
         if (i < s1) {
           const float w = weight_rn(g, ajv[u]);
 #pragma unroll

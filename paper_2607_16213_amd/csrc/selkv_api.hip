@@ -18,6 +18,7 @@ selkv_status make_shape(const selkv_params* p, Shape* s) {
   if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
   if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || p->seq_len < 1) return SELKV_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+  if (p->seq_len > (1 << 28)) return SELKV_EUNSUPPORTED;   // per-head arrays addressed by 32-bit byte offsets
   if (p->window < 1 || p->window > p->seq_len) return SELKV_EINVAL;
   if (p->pool_kernel < 1 || (p->pool_kernel % 2) == 0) return SELKV_EINVAL;
   if (p->pool_kernel > 1025) return SELKV_EUNSUPPORTED;

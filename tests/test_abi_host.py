@@ -98,6 +98,8 @@ def test_validation_codes(S):
     assert st(S.params(seq_len=3, window=3, budget_ratio=0.25)) == 1   # m = 0
     assert st(S.params(seq_len=100, gate_temperature=0.0)) == 1
     assert st(S.params(seq_len=100, bucket=65)) == 3
+    assert st(S.params(seq_len=(1 << 28) + 1)) == 3
+    assert st(S.params(seq_len=1 << 28)) == 0
     assert st(S.params(seq_len=100, group=9), S.CALL_DECODE) == 1
     p = S.params(seq_len=100)
     p.struct_size = 4
