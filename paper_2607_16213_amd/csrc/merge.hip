@@ -529,14 +529,16 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
   }
   const bool routed = t_e >= 0;
   // rank by (target, lane); unrouted lanes after every routed one
+  // (routed lanes all lie below ne, so both loops stop there: a routed
+  // lane's rank and the source of every rank below nrouted are exact)
   const int key = routed ? t_e : 0x7fffffff;
   int rank = 0;
-  for (int q = 0; q < 64; ++q) {
+  for (int q = 0; q < ne; ++q) {
     const int kq = __builtin_amdgcn_readlane(key, q);
     rank += (kq < key || (kq == key && q < lane)) ? 1 : 0;
   }
   int src = 0;   // the lane whose rank is this lane
-  for (int q = 0; q < 64; ++q)
+  for (int q = 0; q < ne; ++q)
     if (__builtin_amdgcn_readlane(rank, q) == lane) src = q;
   const int nrouted = __popcll(__ballot(routed));
   const int s_t = __shfl(t_e, src, 64), s_pos = __shfl(pos_e, src, 64);
@@ -599,7 +601,7 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
             for (int e = 0; e < E; ++e) kacc[e] = fmaf(w, kre[u].get(e), kacc[e]);
           }
           wsum += w;
-          if (col == 0) gh[ev[u]] = g;
+          if (col == 0) store_u32off(gh, (uint32_t)ev[u], g);
         }
       }
     }
