@@ -10,9 +10,12 @@
  *        target [B,H,n-m]; float32 gate [B,H,n-m], K_out [B,H,m,d],
  *        V_out [B,H,m,d], bias [B,H,m], out [B,H*G,d], attn [B,H,n],
  *        score [B,H,n-m_r']
+ * It then runs the fused selkv_merge_bias into fresh buffers and checks that
+ * it reproduces the separate merge and bias bit for bit.
  * Exits 0 on success; on failure prints the failing call and its status. */
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include "selkv.h"
 
@@ -125,7 +128,35 @@ int main(int argc, char** argv) {
   SELKV_OK_(selkv_merge(&p, K, V, attn, vnorm, kept, evicted, K_out, V_out, target, gate, ws, ws_bytes, st));
   SELKV_OK_(selkv_bias(&p, attn, kept, evicted, target, gate, bias, ws, ws_bytes, st));
   SELKV_OK_(selkv_decode_attn(&p, q, K_out, V_out, bias, (int32_t)m, out, ws, ws_bytes, st));
+
+  /* the fused call must reproduce selkv_merge + selkv_bias bit for bit */
+  void* K_out2 = dev_alloc(B * H * m * d * sizeof(float));
+  void* V_out2 = dev_alloc(B * H * m * d * sizeof(float));
+  int32_t* target2 = (int32_t*)dev_alloc(B * H * ne * sizeof(int32_t));
+  float* gate2 = (float*)dev_alloc(B * H * ne * sizeof(float));
+  float* bias2 = (float*)dev_alloc(B * H * m * sizeof(float));
+  SELKV_OK_(selkv_workspace_size(&p, SELKV_CALL_MERGE_BIAS, 0, &sz));
+  if (sz > ws_bytes) return 6;
+  SELKV_OK_(selkv_merge_bias(&p, K, V, attn, vnorm, kept, evicted, K_out2, V_out2, target2, gate2, bias2, ws,
+                             ws_bytes, st));
   HIP_OK(hipStreamSynchronize(st));
+  const struct { const void *a, *b; size_t bytes; const char* name; } same[] = {
+      {K_out, K_out2, B * H * m * d * sizeof(float), "K_out"}, {V_out, V_out2, B * H * m * d * sizeof(float), "V_out"},
+      {target, target2, B * H * ne * sizeof(int32_t), "target"}, {gate, gate2, B * H * ne * sizeof(float), "gate"},
+      {bias, bias2, B * H * m * sizeof(float), "bias"}};
+  for (size_t i = 0; i < sizeof(same) / sizeof(same[0]); ++i) {
+    char* ha = (char*)malloc(same[i].bytes > 0 ? same[i].bytes : 1);
+    char* hb = (char*)malloc(same[i].bytes > 0 ? same[i].bytes : 1);
+    if (!ha || !hb) return 5;
+    HIP_OK(hipMemcpy(ha, same[i].a, same[i].bytes, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hb, same[i].b, same[i].bytes, hipMemcpyDeviceToHost));
+    if (memcmp(ha, hb, same[i].bytes) != 0) {
+      fprintf(stderr, "selkv_merge_bias differs from selkv_merge + selkv_bias in %s\n", same[i].name);
+      return 7;
+    }
+    free(ha);
+    free(hb);
+  }
 
   FILE* o = fopen(argv[2], "wb");
   if (!o) return 1;
@@ -144,7 +175,8 @@ int main(int argc, char** argv) {
   fclose(o);
 
   HIP_OK(hipStreamDestroy(st));
-  void* bufs[] = {K, V, Q, q, score, attn, vnorm, kept, evicted, target, gate, K_out, V_out, bias, out, ws};
+  void* bufs[] = {K, V, Q, q, score, attn, vnorm, kept, evicted, target, gate, K_out, V_out, bias, out, ws,
+                  K_out2, V_out2, target2, gate2, bias2};
   for (size_t i = 0; i < sizeof(bufs) / sizeof(bufs[0]); ++i) HIP_OK(hipFree(bufs[i]));
   free(hK);
   free(hV);
