@@ -50,6 +50,8 @@ def parse():
                     help="layers timed with the all-pairs cosine routing variant (0 = skip)")
     ap.add_argument("--no-generation", action="store_true", help="skip the growing-cache generation loop timing")
     ap.add_argument("--no-rope", action="store_true", help="skip the RoPE repositioning timing")
+    ap.add_argument("--no-batched-decode", action="store_true",
+                    help="skip the all-layers-in-one-call decode timing (profiles of the per-layer call)")
     ap.add_argument("--no-union", action="store_true",
                     help="skip the timings of the alternative modes (GQA union, nearest-kept fallback, merged keys)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -531,7 +533,8 @@ def main():
         out["full_cache_decode_GBs"] = round(full_decode_bytes / (full_us * 1e-6) / 1e9, 1)
         out["decode_speedup_vs_full_cache"] = round(full_us / dec_us, 3)
 
-    out["batched_decode"] = measure_batched_decode(job)
+    if not args.no_batched_decode:
+        out["batched_decode"] = measure_batched_decode(job)
     if not args.no_generation:
         out["generation_loop"] = measure_generation(job)
     if args.full_cosine_layers > 0:
