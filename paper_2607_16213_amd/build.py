@@ -31,10 +31,14 @@ COMMON_FLAGS = [
 ]
 
 
-# per-file additions: the all-pairs cosine match keeps its MFMA accumulators
-# in ordinary VGPRs, so the fused argmax epilogue reads them without copies
+# per-file additions: kernels whose MFMA results feed VALU work at once (the
+# cosine match's argmax epilogue, the score passes' exponentials, the
+# co-attention probabilities) keep the accumulators in ordinary VGPRs, so
+# nothing is copied out of accumulation registers
 EXTRA_FLAGS = {
     "cosine.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "score.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "coattn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 
 
