@@ -1121,3 +1121,45 @@ def test_select_threshold_bin_staged_or_not(S, kind):
         k_ref, e_ref = O.select(s[h].astype(np.float64), n, m, mr)
         assert np.array_equal(kept[0, h].cpu().numpy(), k_ref), (kind, h)
         assert np.array_equal(ev[0, h].cpu().numpy(), e_ref), (kind, h)
+
+
+# ------------------------------------------------------------------ random configurations, stage by stage
+def _random_config(seed):
+    rng = np.random.default_rng(9000 + seed)
+    d = int(rng.choice([64, 128]))
+    n = int(rng.integers(40, 900))
+    W = int(rng.integers(1, min(64, n) + 1))
+    G = int(rng.choice([1, 2, 3, 4, 5, 8]))
+    case = dict(batch=int(rng.integers(1, 3)), H=int(rng.integers(1, 4)), G=G, d=d, n=n, W=W,
+                dtype=str(rng.choice(["fp32", "bf16"])))
+    kw = dict(bucket=int(rng.choice([1, 3, 8, 16, 32, 48, 64])), pool_kernel=int(rng.choice([1, 3, 5, 9, 33])),
+              recent=int(rng.integers(0, 33)), budget_ratio=float(rng.uniform(max(2.0 / n, 0.02), 1.0)),
+              gate_mode=int(rng.integers(0, 3)), gate_threshold=float(rng.choice([0.0, 0.2, 0.5])),
+              gate_temperature=float(rng.choice([0.25, 0.5, 1.0, 2.0])), alpha=float(rng.uniform(0.1, 2.0)),
+              scale=float(rng.choice([0.0, 0.05, 0.2])))
+    return case, kw
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_random_configs_stagewise(S, seed):
+    """Randomly drawn shapes and parameters (batch, heads, group, d, n, W,
+    bucket, pooling kernel, recent window, budget, gate mode / threshold /
+    temperature, alpha, softmax scale, storage dtype): every stage fed the
+    oracle's inputs matches it (indices bit-exact), one decode step over the
+    oracle's cache matches, and the fused merge + bias call reproduces the
+    separate calls bit for bit on the GPU's own chain."""
+    case, kw = _random_config(seed)
+    print(f"random config {seed}: {case} {kw}", flush=True)
+    t = synth.random_case(seed * 31 + 7, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=5, device=DEV)
+    p = make_params(S, case, **kw)
+    _, chains = run_stagewise(S, p, t["K"], t["V"], t["Qwin"])
+    run_decode_check(S, p, chains, t["K"], steps=1, seed=seed)
+    comp = S.Compressor(p, DEV)
+    comp.run(t["K"], t["V"], t["Qwin"], fused=False)
+    sep = {k: v.clone() for k, v in comp.outputs().items()}
+    comp.run(t["K"], t["V"], t["Qwin"], fused=True)
+    torch.cuda.synchronize()
+    for k, v in comp.outputs().items():
+        assert torch.equal(v, sep[k]), k
