@@ -49,6 +49,31 @@ def case_from_workload(w: synth.Workload, **over):
                 dtype=w.dtype, **over)
 
 
+def random_mode_cases(kind, count):
+    """`count` randomly drawn cases for one of the alternative modes: shapes,
+    budget, bucket and gate parameters vary; the mode fields fit the kind."""
+    out = []
+    for i in range(count):
+        rng = np.random.default_rng({"readings": 101, "fullcos": 202, "union": 303, "coattn": 404}[kind] * 1000 + i)
+        n = int(rng.integers(60, 900))
+        case = dict(batch=int(rng.integers(1, 3)), H=int(rng.integers(2 if kind == "union" else 1, 5)),
+                    G=int(rng.choice([1, 2, 3, 4, 8])), d=int(rng.choice([64, 128])), n=n,
+                    W=int(rng.integers(1, min(48, n) + 1)), dtype=str(rng.choice(["fp32", "bf16"])),
+                    budget_ratio=float(rng.uniform(max(2.0 / n, 0.03), 0.8)), gate_mode=int(rng.integers(0, 3)),
+                    gate_threshold=float(rng.choice([0.0, 0.3])), gate_temperature=float(rng.choice([0.5, 1.0])))
+        if kind == "readings":
+            case.update(route_mode=str(rng.choice(["bucket_nearest", "bucket"])), bucket=int(rng.choice([2, 4, 8, 32])))
+            case["merge_keys"] = 1 if case["route_mode"] == "bucket" else int(rng.integers(0, 2))
+            if case["route_mode"] == "bucket_nearest":   # small buckets, low budget: empty buckets occur
+                case.update(bucket=int(rng.choice([2, 4])), budget_ratio=float(rng.uniform(max(2.0 / n, 0.03), 0.12)))
+        elif kind == "union":
+            case.update(bucket=int(rng.choice([4, 16, 32, 64])))
+        elif kind == "coattn":
+            case.update(bucket=int(rng.choice([8, 16, 20, 32, 64])))
+        out.append(case)
+    return out
+
+
 def oracle_chain(K64, V64, Q64, p, gate_mode):
     """The oracle's steps for one head, chaining fp32-rounded values between
     steps exactly as they are handed to the GPU stage calls."""
@@ -431,6 +456,7 @@ FULLCOS = [
     dict(batch=1, H=1, G=2, d=64, n=100, W=8, dtype="fp32", budget_ratio=0.05),       # m < 16: one partial tile
     dict(batch=1, H=1, G=2, d=64, n=20000, W=32, dtype="bf16", budget_ratio=0.9),     # m > 16384 cursor slots
 ]
+FULLCOS += random_mode_cases("fullcos", 8)
 
 
 @pytest.mark.parametrize("case", FULLCOS, ids=[f"fullcos{i}" for i in range(len(FULLCOS))])
@@ -529,6 +555,7 @@ UNION = [
     dict(batch=1, H=2, G=2, d=64, n=400, W=32, dtype="bf16", route_mode="full_cosine"),
     dict(batch=1, H=4, G=2, d=64, n=256, W=32, dtype="fp32", budget_ratio=1.0),         # nothing evicted
 ]
+UNION += random_mode_cases("union", 8)
 
 
 @pytest.mark.parametrize("case", UNION, ids=[f"union{i}" for i in range(len(UNION))])
@@ -785,6 +812,7 @@ READINGS = [
     dict(batch=1, H=2, G=2, d=128, n=640, W=16, dtype="bf16", route_mode="bucket_nearest", bucket=4,
          budget_ratio=0.1, merge_keys=1),
 ]
+READINGS += random_mode_cases("readings", 8)
 
 
 @pytest.mark.parametrize("case", READINGS, ids=[f"reading{i}" for i in range(len(READINGS))])
@@ -895,6 +923,7 @@ COATTN = [
     dict(batch=1, H=2, G=2, d=128, n=400, W=8, dtype="fp32", bucket=16, budget_ratio=0.05, gate_mode=1),
     dict(batch=1, H=1, G=2, d=64, n=200, W=8, dtype="fp32", budget_ratio=1.0),       # nothing evicted
 ]
+COATTN += random_mode_cases("coattn", 8)
 COATTN_NEAR_TIE = 1e-4   # relative gap of two co-attentions below which fp32 may pick either
 
 
