@@ -39,6 +39,8 @@
 namespace selkv {
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kThreads = 256;          // 4 waves
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxChunkKeys = 4096;   // LDS column accumulator bound
@@ -694,16 +696,17 @@ __global__ __launch_bounds__(kThreads, 3) void score_colsum_tiled(ScoreArgs a) {
   const int full_end = min(ke, n - W + 1);
   const float invG = 1.f / (float)a.G;
 
-  // squared value norms: each thread's pieces of a V tile, summed over the
+  // squared value norms: each thread's pieces of a V tile (four bf16 pairs,
+  // each squared and summed by one fp32-accumulating dot2), summed over the
   // NCHUNK consecutive threads that hold one row (fixed order)
   auto vnorms = [&](int tile, const Chunk16 (&v)[Geo::LPT], bool live) {
 #pragma unroll
     for (int j = 0; j < Geo::LPT; ++j) {
       float ss = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = Elem<bf16_t>::get(v[j], e);
-        ss = fmaf(x, x, ss);
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 x = __builtin_bit_cast(bf16x2, v[j].w[e]);
+        ss = __builtin_amdgcn_fdot2_f32_bf16(x, x, ss, false);
       }
 #pragma unroll
       for (int o = Geo::NCHUNK / 2; o >= 1; o >>= 1) ss += xor_shfl(ss, o);
