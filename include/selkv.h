@@ -28,6 +28,10 @@
  *    kernel surface at the caller's next synchronisation.
  *  - Every call is deterministic: the same inputs give bitwise-identical
  *    outputs (no floating-point atomics).
+ *  - Index inputs (kept_idx, evicted_idx, target) are meant to come from the
+ *    library's own calls.  Positions are clamped into [0, n) and target slots
+ *    checked against [0, m) before any memory access, so a malformed list
+ *    gives wrong outputs but never an access outside the caller's buffers.
  *  - No C++ exception crosses this interface.
  */
 #ifndef SELKV_H_

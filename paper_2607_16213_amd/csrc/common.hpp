@@ -142,6 +142,13 @@ struct RawSlice {
   }
 };
 
+// A token position read from a kept / evicted list, clamped into [0, n): a
+// list that breaks its contract (say, not produced by selkv_select) gives
+// wrong results but never an access outside the cache.
+__device__ __forceinline__ int clamp_pos(int32_t p, int n) {
+  return (int)min((uint32_t)p, (uint32_t)(n - 1));
+}
+
 // A value every lane of the wave holds alike, moved to a scalar register.
 __device__ __forceinline__ float uniform(float v) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));

@@ -64,7 +64,7 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     const int e = min(r0 + rb * 16 + col, ne - 1);
-    const int pos = eh[e];
+    const int pos = clamp_pos(eh[e], n);
 #pragma unroll
     for (int c = 0; c < NCH; ++c) q[rb][c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
   }
@@ -76,7 +76,7 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = min(r0 + rb * 16 + grp * 4 + i, ne - 1);
-      const float vn = vnh[eh[e]];
+      const float vn = vnh[clamp_pos(eh[e], n)];
       inv_j[rb][i] = vn > 0.f ? 1.f / vn : 0.f;
       best[rb][i] = kNegInf;
       bidx[rb][i] = 0;
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
   Chunk16 kcur[NCH], knxt[NCH];
   float icur, inxt;
   {
-    const int pos = kh[min(col, m - 1)];
+    const int pos = clamp_pos(kh[min(col, m - 1)], n);
 #pragma unroll
     for (int c = 0; c < NCH; ++c) kcur[c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
     const float vn = vnh[pos];
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
   }
   for (int t = 0; t < m; t += 16) {
     {
-      const int pos = kh[min(t + 16 + col, m - 1)];
+      const int pos = clamp_pos(kh[min(t + 16 + col, m - 1)], n);
 #pragma unroll
       for (int c = 0; c < NCH; ++c) knxt[c] = load16(Vh + (size_t)pos * RB + (c * 4 + grp) * 16);
       const float vn = vnh[pos];
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   Chunk16 q[NRB][NCH];
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
-    const int pos = eh[min(r0 + rb * 16 + col, ne - 1)];
+    const int pos = clamp_pos(eh[min(r0 + rb * 16 + col, ne - 1)], n);
 #pragma unroll
     for (int c = 0; c < NCH; ++c) q[rb][c] = load16(Vh + (size_t)pos * Geo::RB + (c * 4 + grp) * 16);
   }
@@ -243,9 +243,9 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     for (int j = 0; j < LPT; ++j) {
       int row, ch;
       dma_piece<D>(j, wave, lane, row, ch);
-      ix[slot][j] = kh[min(tile * kMT + row, m - 1)];
+      ix[slot][j] = clamp_pos(kh[min(tile * kMT + row, m - 1)], n);
     }
-    ixn[slot] = kh[min(tile * kMT + (tid & (kMT - 1)), m - 1)];
+    ixn[slot] = clamp_pos(kh[min(tile * kMT + (tid & (kMT - 1)), m - 1)], n);
   };
   // past the end the loads re-read the last kept row (masked by s_off), so
   // every trip issues the same loads
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     for (int rb = 0; rb < NRB; ++rb) {
       const int e = r0 + rb * 16 + col;
       if (e < ne) {
-        const float vn = vnh[eh[e]];
+        const float vn = vnh[clamp_pos(eh[e], n)];
         const float cosv = vn > 0.f ? best[rb] * (1.f / vn) : 0.f;
         float g;
         if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
@@ -499,7 +499,7 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
   const int32_t* oh = a.off + (size_t)head * (m + 1);
   const int32_t* lh = a.list + (size_t)head * ne;
   const float* ah = a.attn + (size_t)head * n;
-  const int pos = kh[s];
+  const int pos = clamp_pos(kh[s], n);
   const int l0 = oh[s], l1 = oh[s + 1];
   const float a_s = ah[pos];
 
@@ -516,7 +516,7 @@ __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a)
     float w = 0.f;
     if (li < l1) {
       const int e = lh[li];
-      jp = eh[e];
+      jp = clamp_pos(eh[e], n);
       w = weight_rn(gh[e], ah[jp]);
     }
     const int cnt = min(64, l1 - lb);

@@ -251,11 +251,11 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
   int pos_k = 0, pos_e = 0;
   float a_k = kNegInf, a_e = 0.f, vn_e = 0.f;
   if (lane < nk) {
-    pos_k = kh[k0 + lane];
+    pos_k = clamp_pos(kh[k0 + lane], n);
     a_k = ah[pos_k];
   }
   if (lane < ne) {
-    pos_e = eh[e0 + lane];
+    pos_e = clamp_pos(eh[e0 + lane], n);
     a_e = ah[pos_e];
     vn_e = vnh[pos_e];
   }
@@ -516,11 +516,11 @@ __global__ __launch_bounds__(kThreads) void merge_targets_kernel(MergeArgs a) {
   int pos_k = 0, pos_e = 0, t_e = -1;
   float a_k = 1.f, a_e = 0.f, vn_e = 0.f;
   if (lane < nk) {
-    pos_k = kh[k0 + lane];
+    pos_k = clamp_pos(kh[k0 + lane], n);
     a_k = ah[pos_k];
   }
   if (lane < ne) {
-    pos_e = eh[e0 + lane];
+    pos_e = clamp_pos(eh[e0 + lane], n);
     a_e = ah[pos_e];
     vn_e = vnh[pos_e];
     const int t = th[e0 + lane];
@@ -745,8 +745,8 @@ __global__ __launch_bounds__(kThreads) void bias_bucket_kernel(BiasArgs a) {
     const bool has_k = ok[bi] && lane < k1[bi] - k0[bi];
     t_e[bi] = has_e ? th[e0[bi] + lane] : -1;
     g_e[bi] = has_e ? gh[e0[bi] + lane] : 0.f;
-    j_e[bi] = has_e ? eh[e0[bi] + lane] : 0;
-    pos_k[bi] = has_k ? kh[k0[bi] + lane] : 0;
+    j_e[bi] = has_e ? clamp_pos(eh[e0[bi] + lane], n) : 0;
+    pos_k[bi] = has_k ? clamp_pos(kh[k0[bi] + lane], n) : 0;
   }
   float c_e[kBiasBuckets], a_k[kBiasBuckets];
 #pragma unroll
@@ -797,8 +797,8 @@ __global__ __launch_bounds__(kThreads) void bias_nearest_kernel(BiasArgs a) {
   if (k0 >= k1 || k1 > m || e0 < 0 || e0 > e1 || e1 > n - m) return;   // empty bucket or inconsistent list
   const int nk = k1 - k0, ne = e1 - e0;
   const int t_e = lane < ne ? th[e0 + lane] : -1;
-  const float c_e = lane < ne ? weight_rn(gh[e0 + lane], ah[eh[e0 + lane]]) : 0.f;
-  const float a_k = lane < nk ? ah[kh[k0 + lane]] : 1.f;
+  const float c_e = lane < ne ? weight_rn(gh[e0 + lane], ah[clamp_pos(eh[e0 + lane], n)]) : 0.f;
+  const float a_k = lane < nk ? ah[clamp_pos(kh[k0 + lane], n)] : 1.f;
   const int k = k0 + lane;
   // the merge's order: the bucket's own tokens, then the left run, then the right run
   float absorbed = bucket_mass(t_e, c_e, k, ne, lane);
