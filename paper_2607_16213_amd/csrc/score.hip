@@ -457,7 +457,7 @@ constexpr int kTiledRows = 128;
 // Pass 2 keeps its per-key outputs in LDS and writes them once at the end:
 // a global store inside the loop would make every wait for the oldest tile
 // also wait for all younger loads (stores and loads retire out of order).
-constexpr int kColsumChunk = 2048;
+constexpr int kColsumChunk = 4096;
 
 template <int D>
 struct TiledGeo {
