@@ -218,6 +218,8 @@ def cpu_baseline(job, n_heads, dev):
             r = O.compress_head(K, V, Q, window=w.window, budget_ratio=w.budgets[0])
             t_comp += time.perf_counter() - t0
             outs.append((layer, h, r))
+    job.oracle_outs = outs      # compared with the GPU's outputs by parity_sample()
+    with threadpool_limits(1):
         t_dec, nd = 0.0, 0
         for (layer, h, r) in outs:
             for st in range(4):
@@ -237,7 +239,32 @@ def cpu_baseline(job, n_heads, dev):
                   f"(n={w.seq_len}), scaled to {heads_total} slices; decode on {nd} (slice, step) samples",
         "seconds": round(t_comp + t_dec, 2),
         "decode_us_per_layer_step": 1e6 * (t_dec / nd) * w.n_heads_kv,
+        "parity_sample": parity_sample(job),
     }
+
+
+def parity_sample(job):
+    """The GPU's default compression of the whole job against the oracle on
+    the slices cpu_baseline() sampled: the largest relative score and
+    attention errors, and how many slices keep exactly the oracle's set.
+    The parity tests accept selection swaps only between scores closer than
+    max(1e-6, 4 x the score error); score_err_above_1e-6 says when that band
+    is wider than 1e-6."""
+    import numpy as np
+    torch = job.torch
+    job.compress()
+    torch.cuda.synchronize()
+    c, B = job.comp, job.w.batch
+    es, ea, same = 0.0, 0.0, 0
+    for (layer, h, r) in job.oracle_outs:
+        i = layer * B
+        s = c.score[i, h].double().cpu().numpy()
+        a = c.attn[i, h].double().cpu().numpy()
+        es = max(es, float((np.abs(s - r["score"]) / np.maximum(np.abs(r["score"]), 1e-30)).max(initial=0.0)))
+        ea = max(ea, float((np.abs(a - r["attn"]) / np.maximum(np.abs(r["attn"]), 1e-30)).max(initial=0.0)))
+        same += int(np.array_equal(c.kept[i, h].cpu().numpy(), r["kept"]))
+    return {"slices": len(job.oracle_outs), "score_rel_err_max": es, "attn_rel_err_max": ea,
+            "kept_equal_slices": same, "score_err_above_1e-6": bool(es > 1e-6)}
 
 
 def measure(job, steps, warmup):
