@@ -255,16 +255,27 @@ def parity_sample(job):
     job.compress()
     torch.cuda.synchronize()
     c, B = job.comp, job.w.batch
-    es, ea, same = 0.0, 0.0, 0
+    es, ea, same, ties_only = 0.0, 0.0, 0, 0
+    diffs = []
     for (layer, h, r) in job.oracle_outs:
         i = layer * B
         s = c.score[i, h].double().cpu().numpy()
         a = c.attn[i, h].double().cpu().numpy()
         es = max(es, float((np.abs(s - r["score"]) / np.maximum(np.abs(r["score"]), 1e-30)).max(initial=0.0)))
         ea = max(ea, float((np.abs(a - r["attn"]) / np.maximum(np.abs(r["attn"]), 1e-30)).max(initial=0.0)))
-        same += int(np.array_equal(c.kept[i, h].cpu().numpy(), r["kept"]))
+        kept = c.kept[i, h].cpu().numpy()
+        if np.array_equal(kept, r["kept"]):
+            same += 1
+        else:
+            diffs.append((set(kept.tolist()) ^ set(r["kept"].tolist()), r))
+    band = max(1e-6, 4 * es)
+    for (d, r) in diffs:   # every differing position within the band of the selection threshold?
+        ms = r["ms"]
+        thr = np.sort(r["score"])[::-1][ms - 1]
+        ties_only += int(all(abs(r["score"][j] - thr) <= band * abs(thr) for j in d))
     return {"slices": len(job.oracle_outs), "score_rel_err_max": es, "attn_rel_err_max": ea,
-            "kept_equal_slices": same, "score_err_above_1e-6": bool(es > 1e-6)}
+            "kept_equal_slices": same, "kept_differ_by_near_ties_only": ties_only,
+            "near_tie_band": band, "score_err_above_1e-6": bool(es > 1e-6)}
 
 
 def measure(job, steps, warmup):
