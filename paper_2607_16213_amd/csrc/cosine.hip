@@ -15,6 +15,9 @@
 //            keys gathered, values copied bit for bit when nothing is absorbed.
 //   bias     one wave per kept slot: Eq. 6 over the same lists.
 // All results are independent of scheduling.
+#include <algorithm>
+#include <cmath>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -38,9 +41,25 @@ struct MatchArgs {
   const int32_t* evicted;
   int32_t* target;
   float* gate;
+  float* part_best;      // parts > 1: per (head, part, evicted row) best value and slot
+  int32_t* part_slot;
   int n, m, gate_mode;
   float tau, inv_temp;
+  int parts, part_tiles;   // the kept range split into `parts` runs of part_tiles tiles
 };
+
+// Target and gate of evicted entry e from its best value (dot / ||v_i||) and slot.
+__device__ __forceinline__ void write_match(const MatchArgs& a, int64_t head, int e, float best, int slot) {
+  const int n = a.n, ne = n - a.m;
+  const float vn = a.vnorm[(size_t)head * n + clamp_pos(a.evicted[(size_t)head * ne + e], n)];
+  const float cosv = vn > 0.f ? best * (1.f / vn) : 0.f;
+  float g;
+  if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
+  else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
+  else g = fminf(1.f, fmaxf(0.f, (cosv - a.tau) * a.inv_temp));
+  a.target[(size_t)head * ne + e] = slot;
+  a.gate[(size_t)head * ne + e] = g;
+}
 
 // Evicted rows r0 .. r0+63 of one head against every kept row.
 template <typename T, int D>
@@ -212,8 +231,12 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int n = a.n, m = a.m, ne = n - m;
-  const int r0 = (blockIdx.x * kWaves + wave) * NRB * 16;
+  // workgroup x: evicted row block x / parts against the kept tiles of run x % parts
+  const int part = blockIdx.x % a.parts;
+  const int r0 = ((blockIdx.x / a.parts) * kWaves + wave) * NRB * 16;
   const bool active = r0 < ne;
+  const int t_begin = part * a.part_tiles;
+  const int t_end = min((m + kMT - 1) / kMT, t_begin + a.part_tiles);
   const char* Vh = a.V + (size_t)head * n * Geo::RB;
   const float* vnh = a.vnorm + (size_t)head * n;
   const int32_t* kh = a.kept + (size_t)head * m;
@@ -234,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     bidx[rb] = 0;
   }
 
-  const int ntiles = (m + kMT - 1) / kMT;
+  const int ntiles = max(0, t_end - t_begin);   // tiles of this run; tile t is kept tile t_begin + t
   int ix[2][LPT];      // kept positions of this thread's DMA rows, one tile ahead
   int ixn[2];          // kept position of slot tid & (kMT - 1) (its norm), one tile ahead
   float rn = 0.f;
@@ -243,9 +266,9 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     for (int j = 0; j < LPT; ++j) {
       int row, ch;
       dma_piece<D>(j, wave, lane, row, ch);
-      ix[slot][j] = clamp_pos(kh[min(tile * kMT + row, m - 1)], n);
+      ix[slot][j] = clamp_pos(kh[min((t_begin + tile) * kMT + row, m - 1)], n);
     }
-    ixn[slot] = clamp_pos(kh[min(tile * kMT + (tid & (kMT - 1)), m - 1)], n);
+    ixn[slot] = clamp_pos(kh[min((t_begin + tile) * kMT + (tid & (kMT - 1)), m - 1)], n);
   };
   // past the end the loads re-read the last kept row (masked by s_off), so
   // every trip issues the same loads
@@ -260,10 +283,11 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     }
     rn = vnh[ixn[slot]];
   };
+  // slots past the run (the trip an odd tile count adds) or past m are masked
   auto commit_norm = [&](float* sinv, float* soff, int tile) {
     if (tid < kMT) {
       sinv[tid] = rn > 0.f ? 1.f / rn : 0.f;
-      soff[tid] = tile * kMT + tid < m ? 0.f : kNegInf;
+      soff[tid] = (tile < ntiles && (t_begin + tile) * kMT + tid < m) ? 0.f : kNegInf;
     }
   };
   // value = fma(dot, 1 / ||v_i||, off): off = -inf masks slots past the end
@@ -285,7 +309,7 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     const int s0 = kk * 16 + grp * 4;
     const f32x4 inv = *reinterpret_cast<const f32x4*>(sinv + s0);
     const f32x4 off = *reinterpret_cast<const f32x4*>(soff + s0);
-    const int slot0 = tile * kMT + s0;
+    const int slot0 = (t_begin + tile) * kMT + s0;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       const float v0 = fmaf(acc[rb][0], inv[0], off[0]);
@@ -348,23 +372,40 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
       }
     }
   if (grp == 0) {
-    int32_t* th = a.target + (size_t)head * ne;
-    float* gh = a.gate + (size_t)head * ne;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       const int e = r0 + rb * 16 + col;
       if (e < ne) {
-        const float vn = vnh[clamp_pos(eh[e], n)];
-        const float cosv = vn > 0.f ? best[rb] * (1.f / vn) : 0.f;
-        float g;
-        if (a.gate_mode == SELKV_GATE_DROP) g = 0.f;
-        else if (a.gate_mode == SELKV_GATE_MERGE_ALL) g = 1.f;
-        else g = fminf(1.f, fmaxf(0.f, (cosv - a.tau) * a.inv_temp));
-        th[e] = bidx[rb];
-        gh[e] = g;
+        if (a.parts == 1) {
+          write_match(a, head, e, best[rb], bidx[rb]);
+        } else {
+          const size_t o = ((size_t)head * a.parts + part) * ne + e;
+          a.part_best[o] = best[rb];
+          a.part_slot[o] = bidx[rb];
+        }
       }
     }
   }
+}
+
+// The runs' results of every evicted row, merged in run (= slot) order: a
+// strictly larger value replaces the best, so equal values keep the lower slot.
+__global__ __launch_bounds__(kThreads) void match_parts_kernel(MatchArgs a) {
+  const int64_t head = blockIdx.y;
+  const int ne = a.n - a.m;
+  const int e = blockIdx.x * kThreads + threadIdx.x;
+  if (e >= ne) return;
+  float best = kNegInf;
+  int slot = 0;
+  for (int p = 0; p < a.parts; ++p) {
+    const size_t o = ((size_t)head * a.parts + p) * ne + e;
+    const float v = a.part_best[o];
+    if (v > best) {
+      best = v;
+      slot = a.part_slot[o];
+    }
+  }
+  write_match(a, head, e, best, slot);
 }
 
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(int32_t* p, int64_t count) {
@@ -611,6 +652,38 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
+namespace {
+
+// Runs the kept range of the bf16 match is split into.  A match workgroup
+// (one per 256 evicted rows) is long-lived and three fit on each of the 256
+// CUs, so with one run per row block the last round of workgroups can leave
+// most CUs idle.  Between the run count reaching eight rounds and twice that
+// (each run keeping at least 8 tiles), the one whose last round is fullest is
+// taken.  A run past the last tile (possible when the split is fine) does no
+// work and reports -inf, which the merge of the runs skips.
+int match_parts(const Shape& s) {
+  const int64_t ne = s.n - s.m;
+  if (ne <= 0) return 1;
+  const int64_t row_wgs = (ne + kWaves * kMatchTiledRB * 16 - 1) / (kWaves * kMatchTiledRB * 16) * s.heads;
+  const int64_t cap = ((int64_t)s.m + kMT - 1) / kMT / 8;   // runs of at least 8 tiles
+  const int64_t slots = 256 * 3;
+  const int64_t p0 = (8 * slots + row_wgs - 1) / row_wgs;
+  const int64_t lo = std::max<int64_t>(1, std::min(p0, cap)), hi = std::max(lo, std::min(2 * p0, cap));
+  int best = 1;
+  double best_idle = 2.0;
+  for (int64_t p = lo; p <= hi; ++p) {
+    const double rounds = (double)(row_wgs * p) / (double)slots;
+    const double idle = (std::ceil(rounds) - rounds) / std::ceil(rounds);
+    if (idle < best_idle - 1e-9) {
+      best_idle = idle;
+      best = (int)p;
+    }
+  }
+  return best;
+}
+
+}  // namespace
+
 GroupPlan plan_group(const Shape& s) {
   GroupPlan p{};
   const size_t ne = (size_t)(s.n - s.m);
@@ -619,12 +692,20 @@ GroupPlan plan_group(const Shape& s) {
   p.list_off = p.cursor_off;
   p.sink_off = p.list_off + align256((ne > 0 ? ne : 1) * (size_t)s.heads * sizeof(int32_t));
   p.bytes = p.sink_off + align256(64 * sizeof(int32_t));
+  // the match's per-run results come first and are consumed before the grouping starts
+  const int parts = match_parts(s);
+  p.match_parts = parts;
+  if (parts > 1) {
+    p.match_slot_off = align256((size_t)s.heads * parts * ne * sizeof(float));
+    const size_t match_bytes = p.match_slot_off + align256((size_t)s.heads * parts * ne * sizeof(int32_t));
+    p.bytes = std::max(p.bytes, match_bytes);
+  }
   return p;
 }
 
-hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
-                               const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
-                               float* gate, hipStream_t st) {
+hipError_t launch_cosine_match(const Shape& s, const GroupPlan& gp, int dtype, int gate_mode, float tau, float temp,
+                               const void* V, const float* vnorm, const int32_t* kept, const int32_t* evicted,
+                               int32_t* target, float* gate, void* ws, hipStream_t st) {
   const int ne = s.n - s.m;
   if (ne <= 0) return hipSuccess;
   MatchArgs a{};
@@ -639,12 +720,24 @@ hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float t
   a.gate_mode = gate_mode;
   a.tau = tau;
   a.inv_temp = 1.f / temp;
-  const int rows_per_block = kWaves * (dtype == SELKV_BF16 ? kMatchTiledRB : kMatchRowBlocks) * 16;
-  const dim3 grid((ne + rows_per_block - 1) / rows_per_block, (unsigned)s.heads);
+  a.parts = 1;
+  a.part_tiles = (s.m + kMT - 1) / kMT;
   if (dtype == SELKV_BF16) {
+    const int rows_per_block = kWaves * kMatchTiledRB * 16;
+    const int row_blocks = (ne + rows_per_block - 1) / rows_per_block;
+    a.parts = gp.match_parts;
+    a.part_tiles = (a.part_tiles + a.parts - 1) / a.parts;
+    a.part_best = reinterpret_cast<float*>(ws);
+    a.part_slot = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + gp.match_slot_off);
+    const dim3 grid((unsigned)(row_blocks * a.parts), (unsigned)s.heads);
     if (s.d == 128) hipLaunchKernelGGL((cosine_match_tiled<128>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((cosine_match_tiled<64>), grid, dim3(kThreads), 0, st, a);
+    if (a.parts > 1)
+      hipLaunchKernelGGL(match_parts_kernel, dim3((ne + kThreads - 1) / kThreads, (unsigned)s.heads), dim3(kThreads),
+                         0, st, a);
   } else {
+    const int rows_per_block = kWaves * kMatchRowBlocks * 16;
+    const dim3 grid((ne + rows_per_block - 1) / rows_per_block, (unsigned)s.heads);
     if (s.d == 128) hipLaunchKernelGGL((cosine_match_kernel<float, 128>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((cosine_match_kernel<float, 64>), grid, dim3(kThreads), 0, st, a);
   }

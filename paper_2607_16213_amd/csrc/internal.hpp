@@ -43,6 +43,8 @@ struct DecodePlan {
 // Workspace of the grouping by target slot (full-cosine routing).
 struct GroupPlan {
   size_t off_off, cursor_off, list_off, sink_off, bytes;   // sink: stores of lanes with nothing to place
+  int match_parts;          // runs the bf16 match splits the kept range into
+  size_t match_slot_off;    // their per-run results: values at 0, slots at match_slot_off
 };
 
 // Workspace of the GQA union mode: flags, mean keys and the shared set per
@@ -86,9 +88,10 @@ hipError_t launch_coattn_route(const Shape& s, const ScorePlan& sp, int dtype, i
 hipError_t launch_bias_bucket(const Shape& s, int bucket, float alpha, const float* attn, const int32_t* kept,
                               const int32_t* evicted, const int32_t* offs, const int32_t* target,
                               const float* gate, float* bias, bool raw, bool nearest, hipStream_t st);
-hipError_t launch_cosine_match(const Shape& s, int dtype, int gate_mode, float tau, float temp, const void* V,
-                               const float* vnorm, const int32_t* kept, const int32_t* evicted, int32_t* target,
-                               float* gate, hipStream_t st);
+// ws: the grouping workspace (plan gp); the per-run match results use it before the grouping does
+hipError_t launch_cosine_match(const Shape& s, const GroupPlan& gp, int dtype, int gate_mode, float tau, float temp,
+                               const void* V, const float* vnorm, const int32_t* kept, const int32_t* evicted,
+                               int32_t* target, float* gate, void* ws, hipStream_t st);
 hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st);
 // values pass when V_out is set (bias, when also set, from the same sums); bias pass alone otherwise
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,

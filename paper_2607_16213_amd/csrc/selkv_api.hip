@@ -133,10 +133,10 @@ selkv_status run_merge(const selkv_params* p, const Shape& s, const void* K, con
                                           p->alpha, raw, stream));
   }
   // all-pairs routing: match, group by target slot, merge per slot
-  e = launch_cosine_match(s, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm, kept_idx,
-                          evicted_idx, target, gate, stream);
-  if (e != hipSuccess) return SELKV_EHIP;
   const GroupPlan gp = plan_group(s);
+  e = launch_cosine_match(s, gp, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm,
+                          kept_idx, evicted_idx, target, gate, ws, stream);
+  if (e != hipSuccess) return SELKV_EHIP;
   e = launch_group(s, gp, target, ws, stream);
   if (e != hipSuccess) return SELKV_EHIP;
   return hip_status(launch_group_merge(s, gp, p->kv_dtype, K, V, attn, kept_idx, evicted_idx, gate, ws, K_out, V_out,
