@@ -460,6 +460,9 @@ FULLCOS = [
     dict(batch=2, H=1, G=4, d=64, n=9000, W=32, dtype="bf16", budget_ratio=0.3, gate_mode=2),
 ]
 FULLCOS += random_mode_cases("fullcos", 8)
+# larger random cases: at least 1024 kept rows, so the match splits the kept range into runs
+FULLCOS += [dict(c, n=int(3000 + 1700 * i), budget_ratio=0.35 + 0.1 * i, dtype="bf16")
+            for i, c in enumerate(random_mode_cases("fullcos", 12)[8:])]
 
 
 @pytest.mark.parametrize("case", FULLCOS, ids=[f"fullcos{i}" for i in range(len(FULLCOS))])
