@@ -1198,3 +1198,46 @@ def test_random_configs_stagewise(S, seed):
     torch.cuda.synchronize()
     for k, v in comp.outputs().items():
         assert torch.equal(v, sep[k]), k
+
+
+# ------------------------------------------------------------------ all-pairs routing at the full ctx100k size, sampled
+def test_full_cosine_full_size_sampled(S):
+    """a9 at the bench's size: one ctx100k layer (8 KV heads, 76800 evicted x
+    25600 kept rows each, the kept range split into runs).  The GPU's own
+    attn / vnorm / kept / evicted feed the full-cosine merge call; for 512
+    sampled evicted rows of two heads the float64 cosine argmax over all
+    kept rows (lowest slot on ties) must be the GPU's target, except where
+    the two cosines lie within 4e-6 of each other; gates follow the chosen
+    target's cosine."""
+    w = synth.WORKLOADS["ctx100k"]
+    t = synth.make_layer(w, 0, DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case_from_workload(w))
+    comp = S.Compressor(p, DEV).run(K, V, Q)
+    pf = make_params(S, case_from_workload(w), route_mode="full_cosine")
+    ws = S.workspace(pf, S.CALL_MERGE, DEV)
+    K_out, V_out = torch.empty_like(comp.K_out), torch.empty_like(comp.V_out)
+    target, gate = torch.empty_like(comp.target), torch.empty_like(comp.gate)
+    S.merge(pf, K, V, comp.attn, comp.vnorm, comp.kept, comp.evicted, K_out, V_out, target, gate, ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(77)
+    ties = 0
+    for h in (0, 5):
+        kept = comp.kept[0, h].cpu().numpy()
+        ev = comp.evicted[0, h].cpu().numpy()
+        V64 = np64(V[0, h])
+        Vk = V64[kept]
+        nk = np.linalg.norm(Vk, axis=1)
+        rows = rng.choice(len(ev), 512, replace=False)
+        vj = V64[ev[rows]]
+        cos = (vj @ Vk.T) / (np.linalg.norm(vj, axis=1)[:, None] * nk[None, :])
+        ref = cos.argmax(axis=1)                      # first (lowest) slot of the maximum
+        got = target[0, h].cpu().numpy()[rows]
+        g = gate[0, h].cpu().numpy()[rows]
+        for r in range(len(rows)):
+            c_ref, c_got = cos[r, ref[r]], cos[r, got[r]]
+            if got[r] != ref[r]:
+                assert c_got >= c_ref - 4e-6 * abs(c_ref), f"head {h} row {ev[rows[r]]}: {c_got!r} vs {c_ref!r}"
+                ties += 1
+            assert abs(g[r] - min(1.0, max(0.0, c_got))) <= TOL["bf16"], f"gate head {h} row {ev[rows[r]]}"
+    print(f"a9 full size: {ties} near-tie routing differences in 1024 sampled rows")
