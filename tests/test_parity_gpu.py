@@ -1241,3 +1241,53 @@ def test_full_cosine_full_size_sampled(S):
                 ties += 1
             assert abs(g[r] - min(1.0, max(0.0, c_got))) <= TOL["bf16"], f"gate head {h} row {ev[rows[r]]}"
     print(f"a9 full size: {ties} near-tie routing differences in 1024 sampled rows")
+
+
+# ------------------------------------------------------------------ co-attention routing at the full ctx100k size, sampled
+def test_coattn_full_size_sampled(S):
+    """The co-attention route mode at the bench's layer size (8 KV heads of
+    4 query heads, 102400 tokens, W = 32).  The whole pipeline runs on the
+    GPU; for 512 sampled evicted tokens of two heads the float64 argmax over
+    the kept tokens of the token's bucket of sum_r A[r, j] A[r, i] (A over
+    all 4 x 32 window rows, lowest position on ties) must be the GPU's
+    target, except within 1e-4 relative of each other; -1 exactly where the
+    bucket keeps nothing; gates follow the chosen target's value cosine."""
+    w = synth.WORKLOADS["ctx100k"]
+    t = synth.make_layer(w, 0, DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case_from_workload(w), route_mode="coattn")
+    comp = S.Compressor(p, DEV).run(K, V, Q)
+    torch.cuda.synchronize()
+    G, Bk = p.group, p.bucket
+    rng = np.random.default_rng(78)
+    ties = unrouted = 0
+    for h in (2, 7):
+        kept = comp.kept[0, h].cpu().numpy()
+        ev = comp.evicted[0, h].cpu().numpy()
+        tg = comp.target[0, h].cpu().numpy()
+        g = comp.gate[0, h].cpu().numpy()
+        K64, V64 = np64(K[0, h]), np64(V[0, h])
+        A = O.window_attention_group(np64(Q[0, h * G:(h + 1) * G]), K64, oracle_scale(p))
+        rows = np.sort(rng.choice(len(ev), 512, replace=False))
+        by_bucket = {}
+        for slot, i in enumerate(kept):
+            by_bucket.setdefault(int(i) // Bk, []).append(slot)
+        for r in rows:
+            j = int(ev[r])
+            cand = by_bucket.get(j // Bk)
+            if not cand:
+                assert tg[r] == -1, f"head {h} evicted {j}: bucket keeps nothing, target {tg[r]}"
+                assert g[r] == 0.0
+                unrouted += 1
+                continue
+            co = A[:, kept[cand]].T @ A[:, j]
+            ref = cand[int(np.argmax(co))]
+            assert tg[r] in cand, f"head {h} evicted {j}: target {tg[r]} outside its bucket"
+            if tg[r] != ref:
+                c_got = float(A[:, kept[tg[r]]] @ A[:, j])
+                assert abs(c_got - co.max()) <= COATTN_NEAR_TIE * abs(co.max()), f"head {h} evicted {j}"
+                ties += 1
+            g_ref = O.gate(V64, kept, ev[r:r + 1], tg[r:r + 1], GATE[p.gate_mode], float(np.float32(p.gate_threshold)),
+                           float(np.float32(p.gate_temperature)))[0]
+            assert abs(g[r] - g_ref) <= TOL["bf16"], f"gate head {h} evicted {j}"
+    print(f"co-attention full size: {ties} near-tie differences, {unrouted} unrouted in 1024 sampled rows")
