@@ -1291,3 +1291,69 @@ def test_coattn_full_size_sampled(S):
                            float(np.float32(p.gate_temperature)))[0]
             assert abs(g[r] - g_ref) <= TOL["bf16"], f"gate head {h} evicted {j}"
     print(f"co-attention full size: {ties} near-tie differences, {unrouted} unrouted in 1024 sampled rows")
+
+
+# ------------------------------------------------------------------ decode over long, ragged and many-head caches
+LONG_DECODE = [
+    dict(B=1, H=8, G=4, d=128, L=25600, bias=True),      # the 100k point's compressed cache
+    dict(B=1, H=8, G=4, d=128, L=11003, bias=True),      # ragged last chunk
+    dict(B=32, H=8, G=4, d=128, L=3000, bias=True),      # 256 heads: one chunk per head
+    dict(B=1, H=2, G=8, d=64, L=20000, bias=False),
+    dict(B=2, H=4, G=1, d=128, L=9001, bias=True),
+    dict(B=1, H=8, G=3, d=128, L=8300, bias=True),
+]
+
+
+@pytest.mark.parametrize("case", LONG_DECODE, ids=[f"long{i}" for i in range(len(LONG_DECODE))])
+def test_decode_long_caches(S, case):
+    """bf16 decode over long and ragged caches, many heads (one chunk per
+    head), G = 1 .. 8, d = 64 / 128, with and without bias, a few dominant
+    entries: sampled heads against the float64 oracle; bitwise the same over
+    repeated calls, with a workspace first filled with garbage (no
+    initialisation is needed), and over HIP graph replays."""
+    B, H, G, d, L = case["B"], case["H"], case["G"], case["d"], case["L"]
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(L * 7 + H)
+    K = (torch.randn((B, H, L, d), device=DEV, generator=gen) * 0.35).to(torch.bfloat16)
+    V = torch.randn((B, H, L, d), device=DEV, generator=gen).to(torch.bfloat16)
+    bias = None
+    if case["bias"]:
+        bias = torch.rand((B, H, L), device=DEV, generator=gen) * 0.5
+        bias[:, :, ::97] += 4.0                       # a few dominant entries, spread over the chunks
+    q = torch.randn((3, B, H * G, d), device=DEV, generator=gen).to(torch.bfloat16)
+    p = S.params(batch=B, n_heads_kv=H, group=G, head_dim=d, kv_dtype="bf16")
+    dec = S.Decoder(p, L, DEV)
+    outs = torch.empty((3, B, H * G, d), dtype=torch.float32, device=DEV)
+    for i in range(3):
+        dec.run(q[i], K, V, bias, out=outs[i])
+    torch.cuda.synchronize()
+    ref = outs.clone()
+    scale = 1 / math.sqrt(d)
+    rng = np.random.default_rng(L)
+    for b, h in {(0, 0), (B - 1, H - 1), (int(rng.integers(B)), int(rng.integers(H)))}:
+        for i in (0, 2):
+            want = O.decode(np64(q[i][b, h * G:(h + 1) * G]), np64(K[b, h])[None], np64(V[b, h])[None],
+                            None if bias is None else np64(bias[b, h])[None], G, scale)
+            assert_close_rows(np64(outs[i][b, h * G:(h + 1) * G]), want, TOL["bf16"], f"decode b{b} h{h} q{i}")
+    dec.ws.fill_(0xAB)                                 # garbage in the partials
+    for i in range(3):
+        dec.run(q[i], K, V, bias, out=outs[i])
+    torch.cuda.synchronize()
+    assert torch.equal(outs, ref), "decode differs after the workspace was filled with garbage"
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dec.run(q[0], K, V, bias)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(3):
+            dec.run(q[i], K, V, bias, out=outs[i])
+    for rep in range(3):
+        outs.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(outs, ref), f"graph replay {rep}"
+        dec.run(q[1], K, V, None)                      # eager work between replays
+        torch.cuda.synchronize()
