@@ -587,9 +587,8 @@ DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
   ck = (ck + kKeysPerStep - 1) / kKeysPerStep * kKeysPerStep;
   p.chunk = (int)ck;
   p.nsplit = (int)((cache_len + ck - 1) / ck);
-  p.counter_bytes = 0;
   p.ml_bytes = ((size_t)heads * p.nsplit * G * sizeof(float2) + 255) & ~(size_t)255;
-  p.bytes = p.counter_bytes + p.ml_bytes + (((size_t)heads * p.nsplit * G * d * sizeof(float) + 255) & ~(size_t)255);
+  p.bytes = p.ml_bytes + (((size_t)heads * p.nsplit * G * d * sizeof(float) + 255) & ~(size_t)255);
   return p;
 }
 
@@ -616,8 +615,8 @@ hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int strid
   a.V = static_cast<const char*>(V);
   a.bias = bias;
   a.out = out;
-  a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(ws) + p.counter_bytes);
-  a.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + p.counter_bytes + p.ml_bytes);
+  a.part_ml = reinterpret_cast<float2*>(ws);
+  a.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + p.ml_bytes);
   a.L = cache_len;
   a.chunk = p.chunk;
   a.nsplit = p.nsplit;

@@ -35,8 +35,7 @@ struct ScorePlan {
 struct DecodePlan {
   int chunk;            // keys per workgroup (multiple of 32)
   int nsplit;           // workgroups per KV head
-  size_t counter_bytes; // per-head completion counters at the start of the workspace
-  size_t ml_bytes;      // per-chunk (max, sum) partials
+  size_t ml_bytes;      // per-chunk (max, sum) partials, at the start of the workspace
   size_t bytes;
 };
 

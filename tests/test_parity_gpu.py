@@ -404,8 +404,8 @@ def test_abi_errors_with_device_memory(S):
 
 def test_decode_hip_graph_replays_match_eager(S):
     """Decode captured in a HIP graph: every replay (with eager work and
-    synchronisation in between) equals the eager result bitwise; the
-    workspace counters stay consistent across graph and eager launches."""
+    synchronisation in between) equals the eager result bitwise; no state
+    carries over in the workspace between graph and eager launches."""
     w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096)
     t = synth.make_layer(w, 0, DEV)
     p = make_params(S, case_from_workload(w))
