@@ -303,7 +303,8 @@ SELKV_API selkv_status selkv_merge_bias(const selkv_params* p, const void* K, co
  * moves from its original position to the contiguous position s.  RoPE is
  * the rotate-half form: dimension j < d/2 pairs with j + d/2 and turns by
  * position * rope_theta^(-2j/d).  The two rotations are applied as one turn
- * by (s - kept_idx[s]) * rope_theta^(-2j/d), formed and reduced in fp64;
+ * by (s - kept_idx[s]) * rope_theta^(-2j/d), formed in fp64 and reduced
+ * modulo one turn there; sine and cosine of the remainder are fp32;
  * rows already at their slot are left bit for bit.
  * In:  kept_idx [B, H_kv, m] (from selkv_select); rope_theta > 1 (10000 for
  *      Llama 2, 500000 for Llama 3).

@@ -3,10 +3,13 @@
 // Kept slot s of a head holds the key of original position kept[s]; Eq. 7
 // undoes its rotation at kept[s] and applies the one at s.  Rotations about
 // the same planes compose, so each dimension pair (j, j + d/2) turns once, by
-// (s - kept[s]) * theta^(-2j/d).  That angle can reach 1e5 rad, so it is
-// formed and reduced modulo 2 pi in fp64; sin / cos of the reduced angle are
-// fp32.  One thread owns the 16-byte chunk c of the low half of a row and
-// the matching chunk of the high half; the row is rewritten in place.
+// (s - kept[s]) * theta^(-2j/d) radians.  That angle can reach 1e5 rad, so it
+// is formed in fp64 in whole turns (radians / 2 pi) and only the fraction of
+// a turn is kept; the hardware sine and cosine take their argument in turns,
+// so that fraction goes to them directly as fp32 (no further range
+// reduction, no division).  One thread owns the 16-byte chunk c of the low
+// half of a row and the matching chunk of the high half; the row is
+// rewritten in place.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -22,8 +25,10 @@ __global__ __launch_bounds__(kThreads) void rope_reposition_kernel(const int32_t
   constexpr int HALF = D / 2;
   constexpr int TPR = HALF / EPC;                  // threads per row
   constexpr int RB = D * (int)sizeof(T);
-  __shared__ double inv_freq[HALF];
-  for (int j = threadIdx.x; j < HALF; j += kThreads) inv_freq[j] = pow(theta, -2.0 * j / D);
+  // turns per position of pair j: theta^(-2j/d) / (2 pi)
+  constexpr double kInvTwoPi = 0.15915494309189533576888376337251;
+  __shared__ double turns_per_pos[HALF];
+  for (int j = threadIdx.x; j < HALF; j += kThreads) turns_per_pos[j] = pow(theta, -2.0 * j / D) * kInvTwoPi;
   __syncthreads();
   const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const int64_t row = t / TPR;
@@ -34,14 +39,12 @@ __global__ __launch_bounds__(kThreads) void rope_reposition_kernel(const int32_t
   if (delta == 0.0) return;                         // already at its slot
   char* base = K_out + row * RB;
   Chunk16 lo = load16(base + c * 16), hi = load16(base + HALF * sizeof(T) + c * 16);
-  constexpr double kTwoPi = 6.283185307179586476925286766559;
 #pragma unroll
   for (int e = 0; e < EPC; ++e) {
     const int j = c * EPC + e;
-    double ang = delta * inv_freq[j];
-    ang -= kTwoPi * rint(ang / kTwoPi);             // |ang| <= pi
-    float sn, cs;
-    sincosf((float)ang, &sn, &cs);
+    const double turns = delta * turns_per_pos[j];
+    const float frac = (float)(turns - floor(turns));   // [0, 1]: the angle modulo one turn
+    const float sn = __builtin_amdgcn_sinf(frac), cs = __builtin_amdgcn_cosf(frac);
     const float x1 = Elem<T>::get(lo, e), x2 = Elem<T>::get(hi, e);
     Elem<T>::put(lo, e, x1 * cs - x2 * sn);
     Elem<T>::put(hi, e, x2 * cs + x1 * sn);
