@@ -187,14 +187,24 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
   // The kept list index of key j is (keys > T before j) + min(keys == T
   // before j, need), so one block scan of the packed (> T, == T) counts per
   // chunk places every key; its evicted index is j minus that.
+  // The scores of chunk c + 1 are loaded before chunk c is scanned, so each
+  // chunk's memory latency hides behind the previous chunk's scan.
   int run_gt = 0, run_eq = 0;
+  float nxt[kPerThread];
+  auto load_chunk = [&](int base) {
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) nxt[e] = s[min(base + tid * kPerThread + e, n_cand - 1)];   // clamped
+  };
+  if (n_cand > 0) load_chunk(0);
   for (int base = 0; base < n_cand; base += kChunk) {
     uint32_t u[kPerThread];
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) u[e] = order_key(nxt[e]);
+    load_chunk(base + kChunk);   // past the end: re-reads the last score, unused
     int ngt = 0, neq = 0;
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
       const int j = base + tid * kPerThread + e;
-      u[e] = order_key(s[min(j, n_cand - 1)]);   // clamped: no load behind a branch
       ngt += (j < n_cand && u[e] > T) ? 1 : 0;
       neq += (j < n_cand && u[e] == T) ? 1 : 0;
     }
