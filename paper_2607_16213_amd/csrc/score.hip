@@ -426,10 +426,27 @@ __global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* cbuf,
   const int j0 = blockIdx.x * kPoolOut;
   const int h = K / 2;
   const float* c = cbuf + (size_t)head * n;
-  for (int i = threadIdx.x; i < kPoolOut + 2 * h; i += kThreads) {
-    const int jj = j0 - h + i;
-    const float v = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
-    tile[i] = (jj >= 0 && jj < n_cand) ? v : 0.f;
+  if (2 * h < kThreads) {
+    // the usual small K: every thread's loads are issued before any is
+    // stored, so their latencies overlap (kPoolOut / kThreads + 1 each)
+    constexpr int kL = kPoolOut / kThreads + 1;
+    float v[kL];
+#pragma unroll
+    for (int u = 0; u < kL; ++u) {
+      const int jj = j0 - h + threadIdx.x + u * kThreads;
+      v[u] = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
+    }
+#pragma unroll
+    for (int u = 0; u < kL; ++u) {
+      const int i = threadIdx.x + u * kThreads, jj = j0 - h + i;
+      if (i < kPoolOut + 2 * h) tile[i] = (jj >= 0 && jj < n_cand) ? v[u] : 0.f;
+    }
+  } else {
+    for (int i = threadIdx.x; i < kPoolOut + 2 * h; i += kThreads) {
+      const int jj = j0 - h + i;
+      const float v = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
+      tile[i] = (jj >= 0 && jj < n_cand) ? v : 0.f;
+    }
   }
   __syncthreads();
   for (int q = threadIdx.x; q < kPoolOut; q += kThreads) {
