@@ -53,17 +53,33 @@ __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[
 }
 
 // start[head][b] = lower_bound(kept, b * B) for b = 0 .. nb (start[nb] = m).
+// Each thread takes kOffSlots consecutive slots s (their kept positions and
+// the one before them loaded together) and writes the starts of the buckets
+// that begin after kept[s - 1] and at or before kept[s].
+constexpr int kOffSlots = 4;
+
 __global__ __launch_bounds__(kThreads) void bucket_offsets_kernel(const int32_t* kept, int32_t* offs, int m,
                                                                  int nb, int B) {
   const int64_t head = blockIdx.y;
-  const int s = blockIdx.x * blockDim.x + threadIdx.x;
-  if (s > m) return;
+  const int s0 = (blockIdx.x * blockDim.x + threadIdx.x) * kOffSlots;
+  if (s0 > m) return;
   const int32_t* kh = kept + (size_t)head * m;
   int32_t* oh = offs + (size_t)head * (nb + 1);
-  // positions outside [0, n) (a caller error) are clamped so writes stay in [0, nb]
-  const int prev_b = s == 0 ? -1 : min(max(kh[s - 1], 0) / B, nb);
-  const int cur_b = s == m ? nb : min(max(kh[s], 0) / B, nb);
-  for (int b = prev_b + 1; b <= cur_b; ++b) oh[b] = s;
+  // positions outside [0, n) (a caller error) are clamped so writes stay in [0, nb];
+  // loads are clamped to [0, m) and none is made when m = 0
+  int bk[kOffSlots + 1];   // bucket of kept[s0 - 1 + u]; -1 before slot 0, nb at slot m
+#pragma unroll
+  for (int u = 0; u <= kOffSlots; ++u) {
+    const int s = s0 - 1 + u;
+    const int pos = m > 0 ? kh[min(max(s, 0), m - 1)] : 0;
+    bk[u] = s < 0 ? -1 : s >= m ? nb : min(max(pos, 0) / B, nb);
+  }
+#pragma unroll
+  for (int u = 0; u < kOffSlots; ++u) {
+    const int s = s0 + u;
+    if (s > m) break;
+    for (int b = bk[u] + 1; b <= bk[u + 1]; ++b) oh[b] = s;
+  }
 }
 
 struct MergeArgs {
@@ -817,7 +833,8 @@ size_t bucket_offsets_bytes(const Shape& s) {
 }
 
 hipError_t launch_bucket_offsets(const Shape& s, int bucket, const int32_t* kept, int32_t* offs, hipStream_t st) {
-  const dim3 grid((s.m + 1 + kThreads - 1) / kThreads, (unsigned)s.heads);
+  const int per_block = kThreads * kOffSlots;
+  const dim3 grid((s.m + 1 + per_block - 1) / per_block, (unsigned)s.heads);
   hipLaunchKernelGGL(bucket_offsets_kernel, grid, dim3(kThreads), 0, st, kept, offs, s.m, s.nb, bucket);
   return hipGetLastError();
 }
