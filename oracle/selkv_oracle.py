@@ -34,10 +34,9 @@ Readings taken where the paper is silent or garbled:
     heads of one cache, trimmed to m_s by the mean score across KV heads
     (ties to the lower position); since every head contributes m_s tokens
     the union never falls short, so the shared kept set has exactly m
-    entries.  The mean is taken in float32 in head order because it decides
-    integers (which tokens survive) and the GPU decides in float32.  R is
-    averaged across KV heads and alpha * ln(mean R) is shared by them;
-  * RoPE repositioning (Sec. 3.6 last subsection, Eq. 7; off by default):
+    entries.  The mean is the float64 arithmetic mean of the heads' scores.
+    R is averaged across KV heads and alpha * ln(mean R) is shared by them;
+  * RoPE repositioning (Sec. 3.7, Eq. 7; off by default):
     the rotate-half convention (dimension j pairs with j + d/2, frequency
     theta^(-2j/d)), retained key i moves from its position p_old = i to
     p_new = its slot in the compressed cache (0 .. m-1, contiguous);
@@ -169,14 +168,10 @@ def select(s: np.ndarray, n: int, m: int, mr: int):
 
 
 def union_mean_score(s_heads: np.ndarray) -> np.ndarray:
-    """Mean aggregate score across the KV heads of one cache (the trimming
-    key of Sec. 3.3's union selection), in float32: the heads' scores are
-    added in head order and the sum divided by the head count."""
-    s_heads = np.asarray(s_heads, dtype=np.float32)
-    acc = np.zeros(s_heads.shape[1], dtype=np.float32)
-    for h in range(s_heads.shape[0]):
-        acc = (acc + s_heads[h]).astype(np.float32)
-    return (acc / np.float32(s_heads.shape[0])).astype(np.float32)
+    """Mean aggregate score across the KV heads of one cache, the trimming
+    key of Sec. 3.3's union selection: the float64 arithmetic mean over the
+    heads of each candidate's score."""
+    return np.asarray(s_heads, dtype=np.float64).mean(axis=0)
 
 
 def select_union(s_heads: np.ndarray, n: int, m: int, mr: int):
@@ -201,7 +196,7 @@ def select_union(s_heads: np.ndarray, n: int, m: int, mr: int):
     cand = np.flatnonzero(union)
     assert cand.shape[0] >= ms, "each head contributes m_s candidates"
     if cand.shape[0] > ms:
-        mean = union_mean_score(s_heads).astype(np.float64)
+        mean = union_mean_score(s_heads)
         order = np.lexsort((cand, -mean[cand]))      # larger mean first, then lower position
         cand = np.sort(cand[order[:ms]])
     kept = np.concatenate([cand, np.arange(n_cand, n)]).astype(np.int64)
@@ -510,6 +505,54 @@ def compress_head(k, v, q_win_group, *, window=None, pool_kernel=5, recent=16, b
                 k_out=k_out, v_out=v_out, weight=w, bias=bias)
 
 
+def compress_union(k_heads, v_heads, q_heads, *, group: int, window=None, pool_kernel=5, recent=16, bucket=32,
+                   budget_ratio=0.25, alpha=0.5, scale=None, gate_mode="cosine", gate_threshold=0.0,
+                   gate_temperature=1.0, route_mode="bucket"):
+    """GQA union mode for the KV heads of one cache (Sec. 3.3 union
+    paragraph, Sec. 3.6 GQA rule): every head is scored as in Algorithm 1
+    step 1, one kept set is chosen by select_union, then each head routes,
+    gates and merges its own evicted tokens into the shared set, and the
+    bias alpha * ln(mean over heads of R) is shared by the heads.
+    k_heads, v_heads [H, n, d]; q_heads [H*G, W, d].  Returns per-head
+    stacked arrays (kept / evicted / bias shared, repeated per head)."""
+    k_heads = np.asarray(k_heads, dtype=np.float64)
+    v_heads = np.asarray(v_heads, dtype=np.float64)
+    q_heads = np.asarray(q_heads, dtype=np.float64)
+    H, n, d = k_heads.shape
+    W = q_heads.shape[1]
+    if window is not None:
+        assert window == W
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    m, mr, ms = budget(n, budget_ratio, recent)
+    a, vn, s = [], [], []
+    for h in range(H):
+        ah = cumulative_attention(q_heads[h * group:(h + 1) * group], k_heads[h], scale)
+        vh = value_norms(v_heads[h])
+        a.append(ah)
+        vn.append(vh)
+        s.append(pool(contribution(ah, vh)[: n - mr], n - mr, pool_kernel))
+    kept, evicted = select_union(np.stack(s), n, m, mr)
+    targets, gates, k_out, v_out = [], [], [], []
+    for h in range(H):
+        if route_mode == "bucket":
+            tg = route_bucket(a[h], kept, evicted, bucket)
+        elif route_mode == "full_cosine":
+            tg, _ = route_full_cosine(v_heads[h], kept, evicted)
+        else:
+            raise ValueError(route_mode)
+        g = gate(v_heads[h], kept, evicted, tg, gate_mode, gate_threshold, gate_temperature)
+        ko, vo, _ = merge(k_heads[h], v_heads[h], a[h], kept, evicted, tg, g)
+        targets.append(tg)
+        gates.append(g)
+        k_out.append(ko)
+        v_out.append(vo)
+    bias = ratio_bias_union(np.stack(a), kept, evicted, np.stack(targets), np.stack(gates), alpha)
+    return dict(m=m, mr=mr, ms=ms, attn=np.stack(a), vnorm=np.stack(vn), score=np.stack(s),
+                kept=np.stack([kept] * H), evicted=np.stack([evicted] * H), target=np.stack(targets),
+                gate=np.stack(gates), k_out=np.stack(k_out), v_out=np.stack(v_out), bias=np.stack([bias] * H))
+
+
 def compress(K, V, Qwin, *, group: int, **kw):
     """Batched driver: K, V [B, H_kv, n, d]; Qwin [B, H_kv*G, W, d].
     Returns a dict of per-(b, kv-head) stacked outputs."""
@@ -523,6 +566,30 @@ def compress(K, V, Qwin, *, group: int, **kw):
             out[key] = per[0][0][key]
         else:
             out[key] = np.stack([np.stack([per[b][h][key] for h in range(Hkv)]) for b in range(B)])
+    return out
+
+
+def decode_steps(qs: np.ndarray, kc: np.ndarray, vc: np.ndarray, bias, group: int,
+                 scale: float) -> np.ndarray:
+    """decode() for many independent query steps against one compressed
+    cache: qs [T, H_q, d] -> o [T, H_q, d].  Per KV head the T*G query rows
+    form one matrix, so each step's logits are the same q . k products with
+    the bias added, softmax over the m entries, and the weighted sum of
+    values."""
+    qs = np.asarray(qs, dtype=np.float64)
+    kc = np.asarray(kc, dtype=np.float64)
+    vc = np.asarray(vc, dtype=np.float64)
+    T, Hq, d = qs.shape
+    out = np.zeros((T, Hq, d), dtype=np.float64)
+    for kv in range(kc.shape[0]):
+        rows = qs[:, kv * group:(kv + 1) * group, :].reshape(T * group, d)
+        logits = scale * (rows @ kc[kv].T)
+        if bias is not None:
+            logits = logits + np.asarray(bias[kv], dtype=np.float64)[None, :]
+        logits = logits - logits.max(axis=1, keepdims=True)
+        p = np.exp(logits)
+        p /= p.sum(axis=1, keepdims=True)
+        out[:, kv * group:(kv + 1) * group, :] = (p @ vc[kv]).reshape(T, group, d)
     return out
 
 

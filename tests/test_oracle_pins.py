@@ -328,6 +328,26 @@ def test_decode_equals_library_attention_with_additive_bias():
     np.testing.assert_allclose(got0, ref0, rtol=1e-13, atol=1e-14)
 
 
+def test_decode_steps_equals_library_attention_per_step():
+    """The many-step decode is, step by step, softmax(scale q.k + bias) v
+    (torch SDPA in float64 with the bias as a float mask)."""
+    r = rng(10)
+    T, Hkv, G, m, d = 5, 2, 3, 13, 8
+    qs = r.standard_normal((T, Hkv * G, d))
+    kc, vc = r.standard_normal((Hkv, m, d)), r.standard_normal((Hkv, m, d))
+    bias = r.random((Hkv, m)) * 3
+    got = O.decode_steps(qs, kc, vc, bias, G, 0.7)
+    for t in range(T):
+        for h in range(Hkv * G):
+            ref = sdpa64(qs[t, h][None, None], kc[h // G][None], vc[h // G][None], mask=bias[h // G][None, None],
+                         scale=0.7)
+            np.testing.assert_allclose(got[t, h], ref[0, 0], rtol=1e-13, atol=1e-14)
+    got0 = O.decode_steps(qs, kc, vc, None, G, 0.7)
+    ref0 = sdpa64(qs.reshape(T, Hkv, G, d).transpose(1, 0, 2, 3).reshape(Hkv, T * G, d), kc, vc, scale=0.7)
+    np.testing.assert_allclose(got0, ref0.reshape(Hkv, T, G, d).transpose(1, 0, 2, 3).reshape(T, Hkv * G, d),
+                               rtol=1e-13, atol=1e-14)
+
+
 # ---------------------------------------------------------------- whole-pipeline identities
 def test_full_budget_is_identity():
     """rho = 1: S = all positions, E is empty, K~ = K, V~ = V, R = 1, and the
