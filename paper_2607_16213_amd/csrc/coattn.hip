@@ -6,7 +6,7 @@
 // P the softmax window attention (scale, causal mask) of the score pass.
 //
 //   row statistics  the score pass 1 kernels and their combine give every
-//                   window row's exponent offset -M - log2 L over all n keys
+//                   window row's max M and 1/L over all n keys
 //   routing         a workgroup stages one head's window queries and row
 //                   offsets in LDS (when they fit in 32 KB) for its four
 //                   waves; each wave routes eight consecutive buckets of
@@ -14,7 +14,7 @@
 //                   tokens first, then evicted ones.  The K fragments
 //                   of the bucket's keys stay in registers; per 16-row block
 //                   of window rows the logits Q K^T come from MFMA, become
-//                   P = 2^(c2 x - M - log2 L) (0 where masked), and the
+//                   P = 2^(c2 x - M) / L (0 where masked), and the
 //                   Gram blocks C = P^T P that pair an evicted row tile with
 //                   a kept column tile accumulate on fp32 MFMA (at 25%
 //                   retention one kept tile: half of the B x B blocks).  Then
@@ -38,7 +38,7 @@ constexpr int kWaves = kThreads / 64;
 struct CoArgs {
   const char* K;
   const char* Q;
-  const float2* stats;   // per row (-M - log2 L, unused), rpad rows per head
+  const float2* stats;   // per row (-M, 1/L), rpad rows per head
   const int32_t* kept;
   const int32_t* offs;   // bucket offsets into kept
   int32_t* target;
@@ -57,7 +57,7 @@ constexpr int kBucketsPerWave = 8;
 // One bucket: the body of the routing described at the top of the file.
 template <typename T, int D, int NT, bool QL>
 __device__ __forceinline__ void route_bucket(const CoArgs& a, int bucket, int64_t head, int lane,
-                                             const char* q_lds, const float* off_lds) {
+                                             const char* q_lds, const float2* off_lds) {
   constexpr int RB = D * (int)sizeof(T);
   constexpr int NCH = RB / 64;
   constexpr int NCHUNK = RB / 16;
@@ -120,23 +120,24 @@ __device__ __forceinline__ void route_bucket(const CoArgs& a, int bucket, int64_
   };
   auto row_off = [&](int r) {
     if constexpr (QL) return off_lds[r];
-    else return st[r].x;
+    else return st[r];
   };
   // query rows and row statistics of the next 16-row block load while the
   // current block is used (indices clamped; rows past R are masked by off)
   Chunk16 qf[NCH];
-  float offn[4];
+  float2 offn[4];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) qf[c] = q_frag(min(col, R - 1), c);
 #pragma unroll
   for (int i = 0; i < 4; ++i) offn[i] = row_off(min(grp * 4 + i, R - 1));
   for (int rb = 0; rb < nrb; ++rb) {
-    float off[4];
+    float off[4], inv[4];
     int rpos[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = rb * 16 + grp * 4 + i;
-      off[i] = r < R ? offn[i] : kNegInf;
+      off[i] = r < R ? offn[i].x : kNegInf;
+      inv[i] = offn[i].y;
       rpos[i] = win0 + (r < R ? r % a.W : 0);
       offn[i] = row_off(min(r + 16, R - 1));
     }
@@ -160,7 +161,7 @@ __device__ __forceinline__ void route_bucket(const CoArgs& a, int bucket, int64_
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         P[t][i] = (ckey[t] >= 0 && ckey[t] <= rpos[i] && off[i] != kNegInf)
-                      ? fast_exp2(fmaf(x[t][i], a.c2, off[i]))
+                      ? fast_exp2(fmaf(x[t][i], a.c2, off[i])) * inv[i]
                       : 0.f;
     }
     // Gram blocks of evicted row tiles against kept column tiles only
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void coattn_route_kernel(CoArgs a) {
   constexpr int QB = QL ? kQldsBytes : 16;
   constexpr int QR = QL ? kQldsBytes / RB : 1;
   __shared__ __align__(16) char q_lds[QB];   // row r, chunk ch at r * RB + (ch ^ (r mod NCHUNK)) * 16
-  __shared__ float off_lds[QR];
+  __shared__ float2 off_lds[QR];
   const int64_t head = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const char* Qh = a.Q + (size_t)head * a.R * RB;
@@ -233,7 +234,7 @@ __global__ __launch_bounds__(kThreads) void coattn_route_kernel(CoArgs a) {
       const int r = idx / NCHUNK, ch = idx % NCHUNK;
       store16(q_lds + r * RB + ((ch ^ (r % NCHUNK)) * 16), load16(Qh + (size_t)r * RB + ch * 16));
     }
-    for (int r = threadIdx.x; r < a.R; r += kThreads) off_lds[r] = st[r].x;
+    for (int r = threadIdx.x; r < a.R; r += kThreads) off_lds[r] = st[r];
     __syncthreads();
   }
   const int first = (blockIdx.x * kWaves + wave) * kBucketsPerWave;

@@ -6,11 +6,13 @@
 // scale * Q K^T are produced on MFMA (16x16x32 bf16, or 16x16x4 fp32) with
 // Q fragments in registers and K streamed from HBM:
 //   pass 1  per (key chunk, row group): online row max / sum of exp  -> ws
-//   combine per KV head: merge the chunk partials in chunk order     -> ws
-//   pass 2  per key chunk: recompute the logits, normalise, sum the G*W
-//           rows of every key column (a_j, divided by G), value norms from
-//           V, write attn, vnorm and c = a * ||v||
-//   pool    centred K-wide moving average of c over [0, n - m_r')
+//   combine per KV head: merge the chunk partials in chunk order into
+//           (-M, 1/L) per row                                        -> ws
+//   pass 2  per key chunk: recompute the logits, normalise
+//           (2^(x - M) * 1/L), sum the G*W rows of every key column
+//           (a_j, divided by G), value norms from V, write attn, vnorm
+//   pool    centred K-wide moving average of c = a * ||v|| over
+//           [0, n - m_r'), in fp64
 // The attention matrix itself is never stored.
 //
 // bf16 with at most 128 window rows (the shapes of the paper's workloads)
@@ -66,7 +68,6 @@ struct ScoreArgs {
   float* vnorm;
   float2* part;
   float2* stats;
-  float* cbuf;
   int n, W, R, G;
   int chunk_keys, nchunks, rpad, nrg;
   int chunk_keys2;   // shared-tile pass 2
@@ -295,10 +296,12 @@ __global__ __launch_bounds__(kThreads) void score_combine_kernel(ScoreArgs a) {
       for (int u = 0; u < kBatch; ++u)
         if (c0 + u < a.nchunks) lse_merge(M, L, v[u].x, v[u].y);
     }
-    // pass 2 takes p = 2^(x - M) / L as 2^(x + off) with off = -M - log2 L
-    // (-inf for padding rows, whose p is then 0)
-    a.stats[(size_t)head * a.rpad + row] =
-        make_float2((row < a.R && L > 0.f) ? -M - log2f(L) : kNegInf, 0.f);
+    // pass 2 takes p = 2^(x - M) * (1/L): the exponent stays near 0 and 1/L
+    // is one correctly rounded division, so no per-row rounding of log2 L
+    // (about 1e-6 absolute at L ~ 1e5) enters every probability of the row.
+    // Padding rows get (-inf, 0), whose p is then 0.
+    const bool live = row < a.R && L > 0.f;
+    a.stats[(size_t)head * a.rpad + row] = make_float2(live ? -M : kNegInf, live ? 1.f / L : 0.f);
   }
 }
 
@@ -330,11 +333,15 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
     const int row0 = rg * ROWS + half * NRB * 16;
     Chunk16 q[NRB][NCH];
     load_q<T, D, NRB>(Qh, a.R, row0, col, grp, q);
-    float off[NRB][4];             // exponent offset -M - log2 L of each row
+    float off[NRB][4], inv[NRB][4];   // -M and 1/L of each row
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) off[rb][i] = st[row0 + rb * 16 + grp * 4 + i].x;
+      for (int i = 0; i < 4; ++i) {
+        const float2 sv = st[row0 + rb * 16 + grp * 4 + i];
+        off[rb][i] = sv.x;
+        inv[rb][i] = sv.y;
+      }
     // each row half reads its share of every V row once: chunks c with c % RW == half
     const bool norms = rg == 0;
     const int R = a.R;
@@ -365,14 +372,15 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) cs += fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i]));
+          for (int i = 0; i < 4; ++i) cs = fmaf(fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i])), inv[rb][i], cs);
       } else {
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float p = fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i]));
-            cs += row_sees(row0 + rb * 16 + grp * 4 + i, key, R, W, n, ke) ? p : 0.f;
+            const bool vis = row_sees(row0 + rb * 16 + grp * 4 + i, key, R, W, n, ke);
+            cs = fmaf(vis ? p : 0.f, inv[rb][i], cs);
           }
       }
       cs += xor_shfl(cs, 16);
@@ -404,57 +412,61 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
     float ss = vn_l[0][local];
 #pragma unroll
     for (int h = 1; h < RW; ++h) ss += vn_l[h][local];
-    const float vn = sqrtf(ss);
     const size_t o = (size_t)head * n + k;
     a.attn[o] = av;
-    a.vnorm[o] = vn;
-    a.cbuf[o] = av * vn;
+    a.vnorm[o] = sqrtf(ss);
   }
 }
 
-// Centred moving average of width K over the candidate range, zero outside:
-// each workgroup stages its kPoolOut outputs' inputs plus the
-// K - 1 halo values in LDS with coalesced loads (zeros outside [0, n_cand)),
-// then each output sums its K neighbours from LDS in ascending position.
+// Centred moving average of width K over the candidate range, zero outside,
+// of c = a * ||v|| (Eq. 1).  The product of the two fp32 outputs is exact in
+// fp64 and the K-term sum and the division are taken there too, so the score
+// carries one rounding to fp32 beyond the errors of a and ||v||.  Each
+// workgroup stages its kPoolOut outputs' products plus the K - 1 halo values
+// in LDS (zeros outside [0, n_cand)), then each output sums its K
+// neighbours from LDS in ascending position.
 constexpr int kPoolOut = 1024;
 constexpr int kPoolMaxK = 1025;
 
-__global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* cbuf, float* score, int n, int n_cand,
-                                                             int K) {
-  __shared__ float tile[kPoolOut + kPoolMaxK - 1];
+__global__ __launch_bounds__(kThreads) void score_pool_kernel(const float* attn, const float* vnorm, float* score,
+                                                             int n, int n_cand, int K) {
+  __shared__ double tile[kPoolOut + kPoolMaxK - 1];
   const int64_t head = blockIdx.y;
   const int j0 = blockIdx.x * kPoolOut;
   const int h = K / 2;
-  const float* c = cbuf + (size_t)head * n;
+  const float* av = attn + (size_t)head * n;
+  const float* vn = vnorm + (size_t)head * n;
   if (2 * h < kThreads) {
     // the usual small K: every thread's loads are issued before any is
     // stored, so their latencies overlap (kPoolOut / kThreads + 1 each)
     constexpr int kL = kPoolOut / kThreads + 1;
-    float v[kL];
+    float x[kL], y[kL];
 #pragma unroll
     for (int u = 0; u < kL; ++u) {
-      const int jj = j0 - h + threadIdx.x + u * kThreads;
-      v[u] = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
+      const int jj = min(max(j0 - h + (int)threadIdx.x + u * kThreads, 0), n_cand - 1);   // clamped, masked below
+      x[u] = av[jj];
+      y[u] = vn[jj];
     }
 #pragma unroll
     for (int u = 0; u < kL; ++u) {
       const int i = threadIdx.x + u * kThreads, jj = j0 - h + i;
-      if (i < kPoolOut + 2 * h) tile[i] = (jj >= 0 && jj < n_cand) ? v[u] : 0.f;
+      if (i < kPoolOut + 2 * h) tile[i] = (jj >= 0 && jj < n_cand) ? (double)x[u] * (double)y[u] : 0.0;
     }
   } else {
     for (int i = threadIdx.x; i < kPoolOut + 2 * h; i += kThreads) {
       const int jj = j0 - h + i;
-      const float v = c[min(max(jj, 0), n_cand - 1)];   // clamped load, masked below
-      tile[i] = (jj >= 0 && jj < n_cand) ? v : 0.f;
+      const int jc = min(max(jj, 0), n_cand - 1);   // clamped load, masked below
+      const double c = (double)av[jc] * (double)vn[jc];
+      tile[i] = (jj >= 0 && jj < n_cand) ? c : 0.0;
     }
   }
   __syncthreads();
   for (int q = threadIdx.x; q < kPoolOut; q += kThreads) {
     const int j = j0 + q;
     if (j < n_cand) {
-      float sum = 0.f;
+      double sum = 0.0;
       for (int t = 0; t < K; ++t) sum += tile[q + t];
-      score[(size_t)head * n_cand + j] = sum / (float)K;
+      score[(size_t)head * n_cand + j] = (float)(sum / (double)K);
     }
   }
 }
@@ -703,11 +715,16 @@ __global__ __launch_bounds__(kThreads, 3) void score_colsum_tiled(ScoreArgs a) {
 
   Chunk16 q[2][Geo::NCH];
   load_q<bf16_t, D, 2>(Qh, R, row0, col, grp, q);
+  // -M of each of the lane's rows in registers; 1/L read from LDS where it
+  // is used (four consecutive rows per 16-byte read), which keeps the
+  // kernel within the register budget of three workgroups per CU
+  __shared__ __align__(16) float s_inv[kTiledRows];
   float off[2][4];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) off[rb][i] = st[row0 + rb * 16 + grp * 4 + i].x;
+  if (tid < kTiledRows) s_inv[tid] = st[tid].y;   // visible after the stream's first barrier
   const int kb = chunk * a.chunk_keys2;
   const int ke = min(n, kb + a.chunk_keys2);
   const int full_end = min(ke, n - W + 1);
@@ -741,18 +758,22 @@ __global__ __launch_bounds__(kThreads, 3) void score_colsum_tiled(ScoreArgs a) {
       if (active && t < ke) {
         f32x4 acc[2];
         tile_logits<D>(stage, kk, col, grp, q, acc);
+        float4 inv[2];
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) inv[rb] = *reinterpret_cast<const float4*>(&s_inv[row0 + rb * 16 + grp * 4]);
         if (t + 16 <= full_end) {
 #pragma unroll
           for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) cs += fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i]));
+            for (int i = 0; i < 4; ++i) cs = fmaf(fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i])), inv[rb][i], cs);
         } else {
 #pragma unroll
           for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float p = fast_exp2(fmaf(acc[rb][i], a.c2, off[rb][i]));
-              cs += row_sees(row0 + rb * 16 + grp * 4 + i, t + col, R, W, n, ke) ? p : 0.f;
+              const bool vis = row_sees(row0 + rb * 16 + grp * 4 + i, t + col, R, W, n, ke);
+              cs = fmaf(vis ? p : 0.f, inv[rb][i], cs);
             }
         }
         cs += xor_shfl(cs, 16);
@@ -771,11 +792,9 @@ __global__ __launch_bounds__(kThreads, 3) void score_colsum_tiled(ScoreArgs a) {
   });
   __syncthreads();
   for (int k = kb + tid; k < ke; k += kThreads) {
-    const float av = s_out[0][k - kb], vn = s_out[1][k - kb];
     const size_t o = (size_t)head * n + k;
-    a.attn[o] = av;
-    a.vnorm[o] = vn;
-    a.cbuf[o] = av * vn;
+    a.attn[o] = s_out[0][k - kb];
+    a.vnorm[o] = s_out[1][k - kb];
   }
 }
 
@@ -789,7 +808,7 @@ hipError_t launch_t(const Shape& s, const ScorePlan& p, ScoreArgs& a, float* sco
   hipLaunchKernelGGL((score_colsum_kernel<T, D, NRB, RW>), dim3(p.nchunks, (unsigned)s.heads), blk, 0, st, a);
   if (s.n_cand > 0)
     hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kPoolOut - 1) / kPoolOut, (unsigned)s.heads), blk, 0,
-                       st, a.cbuf, score, s.n, s.n_cand, pool_kernel);
+                       st, a.attn, a.vnorm, score, s.n, s.n_cand, pool_kernel);
   return hipGetLastError();
 }
 
@@ -815,7 +834,7 @@ hipError_t launch_tiled(const Shape& s, const ScorePlan& p, ScoreArgs& a, float*
   hipLaunchKernelGGL(score_colsum_tiled<D>, dim3(p.nchunks2, (unsigned)s.heads), blk, 0, st, a);
   if (s.n_cand > 0)
     hipLaunchKernelGGL(score_pool_kernel, dim3((s.n_cand + kPoolOut - 1) / kPoolOut, (unsigned)s.heads), blk, 0,
-                       st, a.cbuf, score, s.n, s.n_cand, pool_kernel);
+                       st, a.attn, a.vnorm, score, s.n, s.n_cand, pool_kernel);
   return hipGetLastError();
 }
 
@@ -846,8 +865,7 @@ ScorePlan plan_score(const Shape& s, int dtype) {
     p.nchunks2 = (int)((s.n + p.chunk_keys2 - 1) / p.chunk_keys2);
     p.part_off = 0;
     p.stats_off = align256((size_t)s.heads * p.nchunks * p.rpad * sizeof(float2));
-    p.c_off = p.stats_off + align256((size_t)s.heads * p.rpad * sizeof(float2));
-    p.bytes = p.c_off + align256((size_t)s.heads * s.n * sizeof(float));
+    p.bytes = p.stats_off + align256((size_t)s.heads * p.rpad * sizeof(float2));
     return p;
   }
   // up to 128 rows per row group (4 row blocks per wave, two waves per tile);
@@ -873,8 +891,7 @@ ScorePlan plan_score(const Shape& s, int dtype) {
 
   p.part_off = 0;
   p.stats_off = align256((size_t)s.heads * p.nchunks * p.rpad * sizeof(float2));
-  p.c_off = p.stats_off + align256((size_t)s.heads * p.rpad * sizeof(float2));
-  p.bytes = p.c_off + align256((size_t)s.heads * s.n * sizeof(float));
+  p.bytes = p.stats_off + align256((size_t)s.heads * p.rpad * sizeof(float2));
   return p;
 }
 
@@ -891,7 +908,6 @@ ScoreArgs make_args(const Shape& s, const ScorePlan& p, float scale, const void*
   char* w = static_cast<char*>(ws);
   a.part = reinterpret_cast<float2*>(w + p.part_off);
   a.stats = reinterpret_cast<float2*>(w + p.stats_off);
-  a.cbuf = reinterpret_cast<float*>(w + p.c_off);
   a.n = s.n;
   a.W = s.W;
   a.R = s.R;
