@@ -151,7 +151,8 @@ SELKV_API selkv_status selkv_budget(const selkv_params* p, int32_t* m, int32_t* 
                                     int32_t* m_select);
 
 /* Bytes of scratch the call `call` (selkv_call) needs for `p`.
- * `cache_len` is used only for SELKV_CALL_DECODE (entries per KV head).
+ * `cache_len` is used only for SELKV_CALL_DECODE (entries per KV head);
+ * the size returned then serves every cache length up to `cache_len`.
  * Host-only. */
 SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call, int32_t cache_len,
                                             size_t* bytes);
@@ -296,7 +297,7 @@ SELKV_API selkv_status selkv_merge_bias(const selkv_params* p, const void* K, co
                                         void* K_out, void* V_out, int32_t* target, float* gate, float* bias,
                                         void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Step 7 of Algorithm 1: RoPE repositioning (Sec. 3.6 last subsection,
+/* Step 7 of Algorithm 1: RoPE repositioning (Sec. 3.7,
  * Eq. 7; the paper leaves it off for long contexts).
  *
  * K~_s = RoPE(RoPE^-1(K_out[s], kept_idx[s]), s): the key in kept slot s

@@ -592,6 +592,20 @@ DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G) {
   return p;
 }
 
+// Workspace that covers plan_decode(heads, L, d, G) for every L <= capacity.
+// Rounding the chunk up to whole steps can only lower the split count below
+// min(ceil(kTargetBlocks / heads), ceil(L / kKeysPerStep), kMaxSplit), and
+// that bound grows with L, so its value at L = capacity is the largest.
+size_t decode_workspace_bound(int64_t heads, int capacity, int d, int G) {
+  int64_t nsplit = (kTargetBlocks + heads - 1) / heads;
+  const int64_t max_split = (capacity + kKeysPerStep - 1) / kKeysPerStep;
+  if (nsplit > max_split) nsplit = max_split;
+  if (nsplit > kMaxSplit) nsplit = kMaxSplit;
+  if (nsplit < 1) nsplit = 1;
+  const size_t ml = ((size_t)heads * nsplit * G * sizeof(float2) + 255) & ~(size_t)255;
+  return ml + (((size_t)heads * nsplit * G * d * sizeof(float) + 255) & ~(size_t)255);
+}
+
 hipError_t launch_decode(int64_t heads, int n_heads_kv, int cache_len, int stride, int d, int G, int dtype,
                          float scale, const DecodePlan& p, const void* q, const void* K, const void* V,
                          const float* bias, float* out, void* ws, hipStream_t st, const void* k_new,

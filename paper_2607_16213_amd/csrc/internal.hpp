@@ -29,7 +29,7 @@ struct ScorePlan {
   int tiled;         // 1: shared-tile passes (bf16, at most 128 window rows)
   int chunk_keys2;   // shared-tile pass 2: keys per workgroup (outputs staged in LDS)
   int nchunks2;      // shared-tile pass 2: chunks per KV head
-  size_t part_off, stats_off, c_off, bytes;
+  size_t part_off, stats_off, bytes;
 };
 
 struct DecodePlan {
@@ -57,6 +57,8 @@ ScorePlan plan_score(const Shape& s, int dtype);
 UnionPlan plan_union(const Shape& s);
 GroupPlan plan_group(const Shape& s);
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G);
+// bytes that cover plan_decode(heads, L, d, G).bytes for every L <= capacity
+size_t decode_workspace_bound(int64_t heads, int capacity, int d, int G);
 size_t bucket_offsets_bytes(const Shape& s);
 
 // Launchers return hipSuccess or the launch error.

@@ -187,7 +187,7 @@ SELKV_API selkv_status selkv_workspace_size(const selkv_params* p, int32_t call,
     if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
     if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || p->group > 8 || cache_len < 1) return SELKV_EINVAL;
     if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
-    *bytes = plan_decode((int64_t)p->batch * p->n_heads_kv, cache_len, p->head_dim, p->group).bytes;
+    *bytes = decode_workspace_bound((int64_t)p->batch * p->n_heads_kv, cache_len, p->head_dim, p->group);
     return SELKV_OK;
   }
   Shape s;

@@ -153,6 +153,34 @@ def test_rope_reposition_validation(S):
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_decode_workspace_covers_every_shorter_cache(S):
+    """The decode workspace sized for a capacity serves every cache length up
+    to it: the size never shrinks as the length grows (so the capacity's
+    size is the largest), for head counts that split the cache into few or
+    many chunks, including a capacity whose rounded chunk count is below
+    that of shorter caches (2175 entries over 8 KV heads)."""
+    for (B, H, G, d) in [(1, 8, 4, 128), (1, 2, 2, 64), (4, 32, 1, 128), (1, 1, 8, 128), (3, 5, 3, 64)]:
+        p = S.params(batch=B, n_heads_kv=H, group=G, head_dim=d, seq_len=64)
+        for cap in (1, 17, 100, 2175, 2176, 4113, 9000):
+            sizes = [S.workspace_bytes(p, S.CALL_DECODE, L) for L in range(1, cap + 1)]
+            assert all(a <= b for a, b in zip(sizes, sizes[1:])), (B, H, cap)
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="fake pointers are only passed where no GPU exists")
+def test_decode_append_accepts_the_capacity_workspace_at_every_length(S):
+    """Every append step of a cache grown up to its capacity passes the
+    workspace check with the size returned for the capacity (the call then
+    fails at the launch, there being no GPU, never with EWORKSPACE)."""
+    fake = ctypes.c_void_p(0x10000)
+    for (H, G, cap) in [(8, 4, 2175), (8, 4, 8191 // 4 + 128), (2, 2, 700), (32, 1, 4096 + 128)]:
+        p = S.params(batch=1, n_heads_kv=H, group=G, head_dim=128, seq_len=64)
+        ws = S.workspace_bytes(p, S.CALL_DECODE, cap)
+        for L in range(0, cap):
+            st = S.lib.selkv_decode_append(ctypes.byref(p), fake, fake, fake, fake, fake, None, L, cap, fake, fake,
+                                           ws, None)
+            assert st != 5, (H, cap, L)
+
+
 def test_decode_append_validation(S):
     p = S.params(seq_len=256)
     fake = ctypes.c_void_p(0x10000)
