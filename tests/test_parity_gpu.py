@@ -4,10 +4,12 @@ the same seeded, storage-rounded inputs.
 Stage-wise checks feed every GPU call the oracle's own inputs for that step
 (so a selection near-tie cannot cascade); end-to-end checks run the whole
 GPU pipeline and allow only selection swaps between near-tied scores.
-Bars: indices and gathered keys bit-exact; score / attn / vnorm within 1e-4
-relative (fp32 arithmetic on exact inputs); merged values, decode outputs and
-gates within 1e-4 (fp32 storage) or 2e-2 (bf16 storage); bias within
-alpha * that tolerance.
+Bars: indices and gathered keys bit-exact, except near-ties within 1e-6
+relative (counted, shown in the session's terminal summary); score / attn /
+vnorm within 1e-4 relative (fp32 arithmetic on exact inputs); gates within
+1e-5 absolute in every dtype (fp32 arithmetic on exact inputs); merged values
+and decode outputs within 1e-4 (fp32 storage) or 2e-2 (bf16 storage); bias
+within alpha * that tolerance.
 """
 import math
 
@@ -17,8 +19,10 @@ import torch
 
 from oracle import selkv_oracle as O
 from paper_2607_16213_amd import synth
-from tests.parity_util import (SCORE_RTOL, TOL, assert_close_elem, assert_close_rows, compare_end_to_end, dtype_name,
-                               np64, oracle_head_score, oracle_scale)
+from tests.parity_util import (GATE, GATE_ATOL, NEAR_TIE, SCORE_RTOL, TOL, assert_close_elem, assert_close_rows,
+                               case_from_workload, compare_end_to_end, dtype_name, gpu_head, layers_batch,
+                               make_params, np64, oracle_chain, oracle_head_score, oracle_scale, record,
+                               union_selection_check)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -34,19 +38,6 @@ def S():
 
 def to_dev(x, dtype):
     return torch.as_tensor(np.ascontiguousarray(x)).to(dtype).to(DEV).contiguous()
-
-
-def make_params(S, w_or_case, **kw):
-    base = dict(batch=w_or_case["batch"], n_heads_kv=w_or_case["H"], group=w_or_case["G"],
-                head_dim=w_or_case["d"], seq_len=w_or_case["n"], window=w_or_case["W"],
-                kv_dtype=w_or_case["dtype"])
-    base.update(kw)
-    return S.params(**base)
-
-
-def case_from_workload(w: synth.Workload, **over):
-    return dict(batch=w.batch, H=w.n_heads_kv, G=w.group, d=w.head_dim, n=w.seq_len, W=w.window,
-                dtype=w.dtype, **over)
 
 
 def random_mode_cases(kind, count):
@@ -72,36 +63,6 @@ def random_mode_cases(kind, count):
             case.update(bucket=int(rng.choice([8, 16, 20, 32, 64])))
         out.append(case)
     return out
-
-
-def oracle_chain(K64, V64, Q64, p, gate_mode):
-    """The oracle's steps for one head, chaining fp32-rounded values between
-    steps exactly as they are handed to the GPU stage calls."""
-    n = K64.shape[0]
-    m, mr, ms = O.budget(n, p.budget_ratio, p.recent)
-    a, vn, s = oracle_head_score(K64, V64, Q64, p)
-    s32 = s.astype(np.float32).astype(np.float64)
-    kept, ev = O.select(s32, n, m, mr)
-    a32 = a.astype(np.float32).astype(np.float64)
-    target = O.route_bucket(a32, kept, ev, p.bucket)
-    g = O.gate(V64, kept, ev, target, gate_mode, float(np.float32(p.gate_threshold)),
-               float(np.float32(p.gate_temperature)))
-    k_out, v_out, _ = O.merge(K64, V64, a32, kept, ev, target, g)
-    g32 = g.astype(np.float32).astype(np.float64)
-    bias = O.ratio_bias(a32, kept, ev, target, g32, float(np.float32(p.alpha)))
-    return dict(a=a, vn=vn, s=s, s32=s32, a32=a32, kept=kept, ev=ev, target=target, g=g, g32=g32,
-                k_out=k_out, v_out=v_out, bias=bias, m=m, mr=mr, ms=ms)
-
-
-GATE = {0: "cosine", 1: "drop", 2: "merge_all"}
-
-
-def gpu_head(comp, b, h):
-    """One (batch, head) slice of the GPU outputs as float64 / int numpy."""
-    return dict(attn=np64(comp.attn[b, h]), score=np64(comp.score[b, h]), kept=comp.kept[b, h].cpu().numpy(),
-                evicted=comp.evicted[b, h].cpu().numpy(), target=comp.target[b, h].cpu().numpy(),
-                gate=np64(comp.gate[b, h]), v_out=np64(comp.V_out[b, h]), bias=np64(comp.bias[b, h]),
-                K_out=np64(comp.K_out[b, h]))
 
 
 def run_stagewise(S, p, K, V, Qwin, heads=None):
@@ -144,7 +105,7 @@ def run_stagewise(S, p, K, V, Qwin, heads=None):
     torch.cuda.synchronize()
     for (b, h), ch in chains.items():
         np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), ch["target"], err_msg=f"target[{b},{h}]")
-        assert np.abs(np64(comp.gate[b, h]) - ch["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert np.abs(np64(comp.gate[b, h]) - ch["g"]).max(initial=0) <= GATE_ATOL, f"gate[{b},{h}]"
         assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(ch["kept"])]), f"K_out[{b},{h}]"
         assert_close_rows(np64(comp.V_out[b, h]), ch["v_out"], tol, f"V_out[{b},{h}]")
     # ---- bias, fed oracle target / gate
@@ -216,16 +177,15 @@ def test_end_to_end_with_near_tie_accounting(S, name):
     torch.cuda.synchronize()
     K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
     tol = TOL[w.dtype]
-    counts = []
     for b in range(w.batch):
         for h in range(w.n_heads_kv):
             ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * w.group:(h + 1) * w.group],
                                  window=w.window, budget_ratio=p.budget_ratio)
             assert_close_elem(np64(comp.attn[b, h]), ch["attn"], SCORE_RTOL, "attn")
             assert_close_elem(np64(comp.score[b, h]), ch["score"], SCORE_RTOL, "score")
-            counts.append(compare_end_to_end(gpu_head(comp, b, h), ch, K64[b, h], w.seq_len, p.bucket, tol,
-                                             float(np.float32(p.alpha))))
-    print(f"{name}: near-tie counts per head: {counts}")
+            counts = compare_end_to_end(gpu_head(comp, b, h), ch, K64[b, h], w.seq_len, p.bucket, tol,
+                                        float(np.float32(p.alpha)))
+            record("end_to_end", f"{name} b{b} h{h}", **counts)
 
 
 # ------------------------------------------------------------------ edge cases, ragged shapes, modes
@@ -262,17 +222,6 @@ def test_edge_cases_stagewise(S, case):
     p = make_params(S, case, **kw)
     _, chains = run_stagewise(S, p, K, V, t["Qwin"])
     run_decode_check(S, p, chains, K, steps=2)
-
-
-def test_mha_sweep_budgets_and_gates(S):
-    """Config-5 shape (MHA, W = 64) at reduced n: every budget, and the 9
-    gate settings on shared scores, stage-wise through merge and bias."""
-    w = synth.WORKLOADS["mha_sweep"].replace(seq_len=2048, batch=2, n_heads_kv=4)
-    t = synth.make_layer(w, 0, DEV)
-    for rho in w.budgets:
-        for (tau, T) in w.gate_sweep:
-            p = make_params(S, case_from_workload(w), budget_ratio=rho, gate_threshold=tau, gate_temperature=T)
-            run_stagewise(S, p, t["K"], t["V"], t["Qwin"], heads=[(0, 0), (1, 3)])
 
 
 # ------------------------------------------------------------------ determinism, bias semantics
@@ -316,55 +265,6 @@ def test_full_budget_identity_on_gpu(S):
     assert torch.equal(a, b)
     ref = O.decode_batched(np64(q), np64(t["K"]), np64(t["V"]), None, 4, 1 / math.sqrt(128))
     assert_close_rows(a.cpu().double().numpy(), ref, TOL["bf16"], "decode")
-
-
-# ------------------------------------------------------------------ full sizes, bench launch configuration
-def _layers(w, n_layers, device):
-    """All layers' caches back to back as one batch [L*B, H, n, d]."""
-    L = n_layers
-    t0 = synth.make_layer(w, 0, device)
-    K = torch.empty((L,) + tuple(t0["K"].shape), dtype=t0["K"].dtype, device=device)
-    V = torch.empty_like(K)
-    Q = torch.empty((L,) + tuple(t0["Qwin"].shape), dtype=t0["Qwin"].dtype, device=device)
-    for layer in range(L):
-        t = t0 if layer == 0 else synth.make_layer(w, layer, device)
-        K[layer], V[layer], Q[layer] = t["K"], t["V"], t["Qwin"]
-    return K.flatten(0, 1), V.flatten(0, 1), Q.flatten(0, 1)
-
-
-@pytest.mark.parametrize("name,samples", [("ctx32k", [(0, 0), (31, 7)]), ("ctx100k", [(0, 3), (31, 6)])])
-def test_full_size_all_layers_sampled(S, name, samples):
-    """The bench's launch: every layer of the cache compressed by one call
-    per step (batch = layers).  Sampled (layer, head) slices are checked
-    end-to-end against the oracle run on that slice alone."""
-    w = synth.WORKLOADS[name]
-    K, V, Q = _layers(w, w.layers, DEV)
-    p = make_params(S, case_from_workload(w), batch=w.layers * w.batch)
-    comp = S.Compressor(p, DEV).run(K, V, Q)
-    torch.cuda.synchronize()
-    tol = TOL[w.dtype]
-    for (layer, h) in samples:
-        K64, V64 = np64(K[layer, h]), np64(V[layer, h])
-        Q64 = np64(Q[layer, h * w.group:(h + 1) * w.group])
-        ch = O.compress_head(K64, V64, Q64, window=w.window, budget_ratio=p.budget_ratio)
-        assert_close_elem(np64(comp.attn[layer, h]), ch["attn"], SCORE_RTOL, "attn")
-        assert_close_elem(np64(comp.vnorm[layer, h]), ch["vnorm"], SCORE_RTOL, "vnorm")
-        s_gpu = np64(comp.score[layer, h])
-        assert_close_elem(s_gpu, ch["score"], SCORE_RTOL, "score")
-        counts = compare_end_to_end(gpu_head(comp, layer, h), ch, K64, w.seq_len, p.bucket, tol,
-                                    float(np.float32(p.alpha)))
-        print(f"{name} layer {layer} head {h}: {counts}")
-        # biased decode on this layer's compressed cache vs the oracle (2 steps)
-        qd = synth.make_decode_queries(w, layer, 2, DEV)
-        dec = S.Decoder(S.params(batch=1, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim,
-                                 kv_dtype=w.dtype), ch["m"], DEV)
-        for st in range(2):
-            out = dec.run(qd[st], comp.K_out[layer:layer + 1], comp.V_out[layer:layer + 1],
-                          comp.bias[layer:layer + 1]).cpu().double().numpy()[0, h * w.group:(h + 1) * w.group]
-            ref = O.decode(np64(qd[st][0, h * w.group:(h + 1) * w.group]), np64(comp.K_out[layer, h])[None],
-                           np64(comp.V_out[layer, h])[None], np64(comp.bias[layer, h])[None], w.group,
-                           1 / math.sqrt(w.head_dim))
-            assert_close_rows(out, ref, tol, "decode")
 
 
 def test_full_cache_decode_100k(S):
@@ -470,9 +370,9 @@ def test_full_cosine_routing_stagewise(S, case):
     """a9: the all-pairs cosine routing on MFMA, the stable grouping by
     target and the segmented merge / bias, each fed the oracle's inputs.
     Target slots must match except where the two best cosines lie within
-    4e-6 of each other (fp32 accumulation over d <= 128 terms of unit-scale
-    products); such rows are counted and their two candidate slots left out
-    of the value checks."""
+    1e-6 of each other relative (fp32 accumulation over d <= 128 terms of
+    unit-scale products); such rows are counted and their two candidate
+    slots left out of the value checks."""
     case = dict(case)
     kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
     t = synth.random_case(case["n"] * 7 + 1, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
@@ -513,13 +413,13 @@ def test_full_cosine_routing_stagewise(S, case):
             vj = V64[b, h][ch["ev"][e]]
             nj = np.linalg.norm(vj)
             cos = lambda s: 0.0 if nk[s] == 0 or nj == 0 else float(vk[s] @ vj) / (nk[s] * nj)
-            assert abs(cos(tg[e]) - cos(target[e])) <= 4e-6, \
-                f"routing differs at evicted {e}: {tg[e]} vs {target[e]}"
+            c1, c2 = cos(tg[e]), cos(target[e])
+            assert abs(c1 - c2) <= NEAR_TIE * max(abs(c1), abs(c2)), \
+                f"routing differs at evicted {e}: {tg[e]} vs {target[e]} (cosines {c1!r}, {c2!r})"
             skip |= {int(tg[e]), int(target[e])}
             ties += 1
         keep_e = np.array([int(target[e]) not in skip for e in range(len(target))], dtype=bool)
-        gate_tol = 8e-6 / float(np.float32(p.gate_temperature))     # cosines agree to ~4e-6
-        assert np.abs(np64(comp.gate[b, h])[keep_e] - g[keep_e]).max(initial=0) <= gate_tol
+        assert np.abs(np64(comp.gate[b, h])[keep_e] - g[keep_e]).max(initial=0) <= GATE_ATOL
         assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(ch["kept"])])
         rows = np.array([s not in skip for s in range(m)], dtype=bool)
         assert_close_rows(np64(comp.V_out[b, h])[rows], v_out[rows], tol, "V_out")
@@ -534,7 +434,7 @@ def test_full_cosine_routing_stagewise(S, case):
     for (b, h), ch in chains.items():
         err = np.abs(np64(comp.bias[b, h]) - ch["fc_bias"]).max(initial=0)
         assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias err {err:.3e}"
-    print(f"full-cosine routing near-ties: {ties}")
+    record("full_cosine_routing_stagewise", case, route_ties=ties)
 
 
 def test_full_cosine_deterministic_and_grouped_in_order(S):
@@ -566,9 +466,11 @@ UNION += random_mode_cases("union", 8)
 
 @pytest.mark.parametrize("case", UNION, ids=[f"union{i}" for i in range(len(UNION))])
 def test_gqa_union_select_merge_bias(S, case):
-    """Union selection fed the oracle's fp32 scores must match bit for bit
-    (the trim mean is fp32 in head order on both sides); merge and the
-    head-averaged bias are then checked per head against the oracle."""
+    """Union selection fed the oracle's fp32 scores must match the oracle's
+    (float64 trim mean) except for near-ties of the trim or of a head's own
+    top-m_s (within 1e-6 relative, counted).  On the GPU's kept set, merge
+    (bucket or full-cosine routing, per head) and the head-averaged bias are
+    then checked per head against the oracle."""
     case = dict(case)
     kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
     t = synth.random_case(case["n"] * 3 + case["H"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
@@ -597,12 +499,17 @@ def test_gqa_union_select_merge_bias(S, case):
     gate_mode = GATE[p.gate_mode]
     alpha = float(np.float32(p.alpha))
     t_in, g_in = comp.target.clone(), comp.gate.clone()
-    want_bias = {}
+    want = {}
+    ties = 0
     for b in range(B):
-        kept, ev = O.select_union(np.stack([heads[(b, h)]["s32"] for h in range(H)]), n, m, mr)
+        kept = comp.kept[b, 0].cpu().numpy()
+        ev = comp.evicted[b, 0].cpu().numpy()
+        s_heads = np.stack([heads[(b, h)]["s32"] for h in range(H)]).astype(np.float64)
+        near, _ = union_selection_check(kept, s_heads, n, m, mr)
+        ties += near
         for h in range(H):
-            np.testing.assert_array_equal(comp.kept[b, h].cpu().numpy(), kept, err_msg=f"kept[{b},{h}]")
-            np.testing.assert_array_equal(comp.evicted[b, h].cpu().numpy(), ev, err_msg=f"evicted[{b},{h}]")
+            np.testing.assert_array_equal(comp.kept[b, h].cpu().numpy(), kept, err_msg=f"shared kept[{b},{h}]")
+            np.testing.assert_array_equal(comp.evicted[b, h].cpu().numpy(), ev, err_msg=f"shared evicted[{b},{h}]")
         tgs, gs = [], []
         for h in range(H):
             hd = heads[(b, h)]
@@ -613,72 +520,114 @@ def test_gqa_union_select_merge_bias(S, case):
             g = O.gate(V64[b, h], kept, ev, tg, gate_mode, float(np.float32(p.gate_threshold)),
                        float(np.float32(p.gate_temperature)))
             g32 = g.astype(np.float32).astype(np.float64)
+            _, v_out, _ = O.merge(K64[b, h], V64[b, h], hd["a32"], kept, ev, tg, g)
+            want[(b, h)] = dict(target=tg, g=g, v_out=v_out, kept=kept, ev=ev)
             tgs.append(tg)
             gs.append(g32)
             t_in[b, h] = torch.as_tensor(tg, dtype=torch.int32)
             g_in[b, h] = torch.as_tensor(g32, dtype=torch.float32)
-        want_bias[b] = O.ratio_bias_union(np.stack([heads[(b, h)]["a32"] for h in range(H)]), kept, ev,
-                                          np.stack(tgs), np.stack(gs), alpha)
-    # merge with the shared set, per head (bucket routing only: full-cosine targets may near-tie)
-    if p.route_mode == 0:
-        S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
-                comp.ws_merge)
-        torch.cuda.synchronize()
-        for b in range(B):
-            kept = comp.kept[b, 0].cpu().numpy()
-            ev = comp.evicted[b, 0].cpu().numpy()
-            for h in range(H):
-                hd = heads[(b, h)]
-                np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), t_in[b, h].cpu().numpy())
-                _, v_out, _ = O.merge(K64[b, h], V64[b, h], hd["a32"], kept, ev, t_in[b, h].cpu().numpy(),
-                                      g_in[b, h].cpu().double().numpy())
-                assert_close_rows(np64(comp.V_out[b, h]), v_out, tol, f"V_out[{b},{h}]")
+        want[b] = O.ratio_bias_union(np.stack([heads[(b, h)]["a32"] for h in range(H)]), kept, ev,
+                                     np.stack(tgs), np.stack(gs), alpha)
+    # merge with the shared set, per head
+    S.merge(p, K, V, a_in, vn_in, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target, comp.gate,
+            comp.ws_merge)
+    torch.cuda.synchronize()
+    route_ties = 0
+    for b in range(B):
+        for h in range(H):
+            r = want[(b, h)]
+            tg = comp.target[b, h].cpu().numpy()
+            skip = set()
+            if p.route_mode == 1:      # all-pairs cosine: near-tied best cosines may pick either slot
+                vk = V64[b, h][r["kept"]]
+                nk = np.linalg.norm(vk, axis=1)
+                for e in np.flatnonzero(tg != r["target"]):
+                    vj = V64[b, h][r["ev"][e]]
+                    nj = np.linalg.norm(vj)
+                    cos = lambda s: 0.0 if nk[s] == 0 or nj == 0 else float(vk[s] @ vj) / (nk[s] * nj)
+                    c1, c2 = cos(tg[e]), cos(r["target"][e])
+                    assert abs(c1 - c2) <= NEAR_TIE * max(abs(c1), abs(c2)), f"routing differs at evicted {e}"
+                    skip |= {int(tg[e]), int(r["target"][e])}
+                    route_ties += 1
+            else:
+                np.testing.assert_array_equal(tg, r["target"], err_msg=f"target[{b},{h}]")
+            keep_e = np.array([int(x) not in skip for x in r["target"]], dtype=bool)
+            assert np.abs(np64(comp.gate[b, h])[keep_e] - r["g"][keep_e]).max(initial=0) <= GATE_ATOL
+            assert torch.equal(comp.K_out[b, h].cpu(), K[b, h].cpu()[torch.as_tensor(r["kept"])])
+            rows = np.array([s not in skip for s in range(m)], dtype=bool)
+            assert_close_rows(np64(comp.V_out[b, h])[rows], r["v_out"][rows], tol, f"V_out[{b},{h}]")
+    # bias fed the oracle's targets and gates
     S.bias(p, a_in, comp.kept, comp.evicted, t_in, g_in, comp.bias, comp.ws_merge)
     torch.cuda.synchronize()
     for b in range(B):
         for h in range(H):
-            err = np.abs(np64(comp.bias[b, h]) - want_bias[b]).max(initial=0)
+            err = np.abs(np64(comp.bias[b, h]) - want[b]).max(initial=0)
             assert err <= max(abs(alpha), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
         assert all(torch.equal(comp.bias[b, 0], comp.bias[b, h]) for h in range(H))
+    record("gqa_union_stagewise", case, selection_swaps=ties, route_ties=route_ties)
+
+
+def union_oracle_compare(S, p, comp, K64, V64, Q64, b, tol):
+    """The GPU's union-mode outputs of cache b against compress_union, head
+    by head (near-ties of the union selection and of routing counted)."""
+    H, G, n = p.n_heads_kv, p.group, p.seq_len
+    m, mr, ms = S.budget(p)
+    route = "full_cosine" if p.route_mode == 1 else "bucket"
+    ref = O.compress_union(K64[b], V64[b], Q64[b], group=G, window=p.window, budget_ratio=p.budget_ratio,
+                           bucket=p.bucket, alpha=float(np.float32(p.alpha)), gate_mode=GATE[p.gate_mode],
+                           gate_threshold=float(np.float32(p.gate_threshold)),
+                           gate_temperature=float(np.float32(p.gate_temperature)), route_mode=route)
+    sel = lambda kept, err: union_selection_check(kept, ref["score"], n, m, mr)
+    totals = {}
+    dirty, skipped = set(), False
+    for h in range(H):
+        ref_h = {k: (v[h] if isinstance(v, np.ndarray) else v) for k, v in ref.items()}
+        vk = None
+        if route == "full_cosine":
+            vk = V64[b, h]
+            nrm = np.linalg.norm(vk, axis=1)
+            key = lambda j, i: 0.0 if nrm[i] == 0 or nrm[j] == 0 else float(vk[i] @ vk[j]) / (nrm[i] * nrm[j])
+        else:
+            key = lambda j, i, a=ref_h["attn"]: a[i]
+        c = compare_end_to_end(gpu_head(comp, b, h), ref_h, K64[b, h], n, p.bucket, tol, float(np.float32(p.alpha)),
+                               route_key=key, local=route != "full_cosine", selection=sel, check_bias=False,
+                               dirty_out=dirty)
+        skipped |= bool(c.get("values_skipped"))
+        for k, v in c.items():
+            totals[k] = max(totals.get(k, 0), v) if k == "score_rel_err" else totals.get(k, 0) + v
+    # the shared bias: every head's ratio enters it, so a near-tie of any head leaves its buckets out
+    gk, rk = comp.kept[b, 0].cpu().numpy(), ref["kept"][0]
+    if not skipped and np.array_equal(gk, rk):
+        alpha = float(np.float32(p.alpha))
+        keep = np.array([int(x) // p.bucket not in dirty for x in gk], dtype=bool)
+        err = np.abs(np64(comp.bias[b, 0])[keep] - ref["bias"][0][keep]).max(initial=0)
+        assert err <= abs(alpha) * tol, f"shared bias err {err:.3e}"
+    elif not skipped:
+        slot_r = {int(x): s for s, x in enumerate(rk)}
+        for s, x in enumerate(gk):
+            if int(x) // p.bucket in dirty or int(x) not in slot_r:
+                continue
+            assert abs(float(comp.bias[b, 0, s]) - ref["bias"][0][slot_r[int(x)]]) <= abs(float(p.alpha)) * tol
+    return totals
 
 
 def test_gqa_union_end_to_end_llama_layer(S):
-    """The whole union-mode compression of a Llama-shaped layer on the GPU.
-    Checked by properties of the GPU's own scores (no oracle input comes from
-    the GPU): one kept set of m entries shared by the eight KV heads; every
-    kept candidate is among some head's top m_s; no union member that was
-    cut has a larger fp32 head-order mean (or an equal mean at a lower
-    position) than a kept one; the shared bias is finite and non-negative."""
+    """The whole union-mode compression of a Llama-shaped layer on the GPU
+    against the oracle's union mode (float64 scores, float64 trim mean):
+    one kept set of m entries shared by the eight KV heads, equal to the
+    oracle's but for near-ties (counted); per-head targets, gates, merged
+    values and the head-averaged bias to their bars."""
     w = synth.WORKLOADS["llama_layer"]
     t = synth.make_layer(w, 0, DEV)
     p = make_params(S, case_from_workload(w), select_mode="union")
     comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
     torch.cuda.synchronize()
     m, mr, ms = S.budget(p)
-    n, H = p.seq_len, p.n_heads_kv
     kept = comp.kept[0].cpu().numpy()
     assert (kept == kept[0]).all(), "all KV heads share one kept set"
-    k0 = kept[0]
-    assert k0.shape[0] == m and (np.diff(k0) > 0).all() and (k0[ms:] == np.arange(n - mr, n)).all()
-    sc = comp.score[0].cpu().numpy()                       # [H, n - mr] fp32
-    pos = np.arange(n - mr)
-    picked = np.zeros(n - mr, dtype=bool)
-    for h in range(H):
-        order = np.lexsort((pos, -sc[h].astype(np.float64)))
-        picked[order[:ms]] = True
-    cand = k0[:ms]
-    assert picked[cand].all()
-    mean = np.zeros(n - mr, dtype=np.float32)
-    for h in range(H):
-        mean = (mean + sc[h]).astype(np.float32)
-    mean = (mean / np.float32(H)).astype(np.float64)
-    cut = np.flatnonzero(picked & ~np.isin(pos, cand))
-    worst_kept = min(zip(mean[cand], -cand))
-    best_cut = max(zip(mean[cut], -cut)) if cut.size else (-np.inf, 0)
-    assert worst_kept > best_cut
-    bias = comp.bias[0]
-    assert all(torch.equal(bias[0], bias[h]) for h in range(H))
-    assert torch.isfinite(bias).all() and (bias >= 0).all()
+    assert all(torch.equal(comp.bias[0, 0], comp.bias[0, h]) for h in range(p.n_heads_kv))
+    counts = union_oracle_compare(S, p, comp, np64(t["K"]), np64(t["V"]), np64(t["Qwin"]), 0, TOL[w.dtype])
+    record("gqa_union_end_to_end", "llama_layer", **counts)
 
 
 # ------------------------------------------------------------------ RoPE repositioning (Eq. 7)
@@ -687,6 +636,9 @@ ROPE = [
     dict(batch=2, H=2, d=128, n=3000, dtype="bf16", theta=500000.0),
     dict(batch=1, H=1, d=128, n=20000, dtype="fp32", theta=10000.0),       # angles up to 1.5e4 rad
     dict(batch=1, H=2, d=64, n=700, dtype="bf16", theta=10000.0, budget_ratio=1.0),
+    # the benchmark's size: a 102400-token layer (25600 kept keys per head), Llama-3 theta
+    dict(batch=1, H=8, d=128, n=102400, dtype="bf16", theta=500000.0),
+    dict(batch=1, H=2, d=128, n=102400, dtype="fp32", theta=500000.0),     # angles up to 1e5 rad
 ]
 
 
@@ -874,7 +826,7 @@ def test_alternative_readings_stagewise(S, case):
     torch.cuda.synchronize()
     for (b, h), r in refs.items():
         np.testing.assert_array_equal(comp.target[b, h].cpu().numpy(), r["target"], err_msg=f"target[{b},{h}]")
-        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= GATE_ATOL, f"gate[{b},{h}]"
         assert_close_rows(np64(comp.V_out[b, h]), r["v_out"], tol, f"V_out[{b},{h}]")
         if mk:
             assert_close_rows(np64(comp.K_out[b, h]), r["k_out"], tol, f"K_out[{b},{h}]")
@@ -890,7 +842,7 @@ def test_alternative_readings_stagewise(S, case):
     for (b, h), r in refs.items():
         err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
         assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
-    print(f"nearest-kept fallbacks: {fallbacks}")
+    record("alternative_readings_stagewise", case, nearest_fallbacks=fallbacks)
 
 
 def test_nearest_fallback_end_to_end_llama_layer(S):
@@ -930,15 +882,14 @@ COATTN = [
     dict(batch=1, H=1, G=2, d=64, n=200, W=8, dtype="fp32", budget_ratio=1.0),       # nothing evicted
 ]
 COATTN += random_mode_cases("coattn", 8)
-COATTN_NEAR_TIE = 1e-4   # relative gap of two co-attentions below which fp32 may pick either
 
 
 @pytest.mark.parametrize("case", COATTN, ids=[f"coattn{i}" for i in range(len(COATTN))])
 def test_coattn_routing_stagewise(S, case):
     """Co-attention routing fed the oracle's kept / evicted lists: every
     target equals the oracle's argmax of sum_r A[r, j] A[r, i] (float64 A)
-    except where the two candidates' co-attentions lie within 1e-4 of each
-    other relative (counted).  Merge and bias with route_mode COATTN are then
+    except where the two candidates' co-attentions lie within 1e-6 of each
+    other relative (NEAR_TIE, counted).  Merge and bias with route_mode COATTN are then
     fed the oracle's targets: gates, merged values (and keys), gathered keys
     and the bias as for the bucket routing."""
     case = dict(case)
@@ -981,7 +932,7 @@ def test_coattn_routing_stagewise(S, case):
             co = lambda s: float(A[:, ch["kept"][s]] @ A[:, j])
             c_gpu, c_ref = co(tg[e]), co(tg_ref[e])
             assert ch["kept"][tg[e]] // p.bucket == j // p.bucket, "target outside the bucket"
-            assert abs(c_gpu - c_ref) <= COATTN_NEAR_TIE * abs(c_ref), f"routing differs at evicted {e}"
+            assert abs(c_gpu - c_ref) <= NEAR_TIE * abs(c_ref), f"routing differs at evicted {e}: {c_gpu!r} {c_ref!r}"
             ties += 1
     # merge / bias fed the oracle's targets
     for (b, h), r in refs.items():
@@ -1001,7 +952,7 @@ def test_coattn_routing_stagewise(S, case):
     assert torch.equal(comp.target, t_in), "merge must not write the given targets"
     for (b, h), r in refs.items():
         ch = r["ch"]
-        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= tol, f"gate[{b},{h}]"
+        assert np.abs(np64(comp.gate[b, h]) - r["g"]).max(initial=0) <= GATE_ATOL, f"gate[{b},{h}]"
         assert_close_rows(np64(comp.V_out[b, h]), r["v_out"], tol, f"V_out[{b},{h}]")
         if mk:
             assert_close_rows(np64(comp.K_out[b, h]), r["k_out"], tol, f"K_out[{b},{h}]")
@@ -1016,14 +967,15 @@ def test_coattn_routing_stagewise(S, case):
     for (b, h), r in refs.items():
         err = np.abs(np64(comp.bias[b, h]) - r["bias"]).max(initial=0)
         assert err <= max(abs(float(np.float32(p.alpha))), 1e-30) * tol, f"bias[{b},{h}] err {err:.3e}"
-    print(f"co-attention routing near-ties: {ties}")
+    record("coattn_routing_stagewise", case, route_ties=ties)
 
 
 def test_coattn_end_to_end_llama_layer(S):
     """The whole pipeline with co-attention routing on a Llama-shaped layer:
     every target lies in its token's bucket, -1 exactly for the buckets that
-    keep nothing, at least one bucket routes differently from Eq. 3, and the
-    run is bitwise repeatable."""
+    keep nothing, at least one bucket routes differently from Eq. 3, the run
+    is bitwise repeatable, and every head matches the oracle's co-attention
+    pipeline end to end (near-ties of selection and routing counted)."""
     w = synth.WORKLOADS["llama_layer"].replace(seq_len=4096, n_heads_kv=4)
     t = synth.make_layer(w, 0, DEV)
     p_co = make_params(S, case_from_workload(w), route_mode="coattn")
@@ -1046,6 +998,18 @@ def test_coattn_end_to_end_llama_layer(S):
             ok = tc[b, h] >= 0
             assert (kept[b, h][tc[b, h][ok]] // Bk == ev[b, h][ok] // Bk).all()
     assert (tc != te).any(), "co-attention should route some token differently from Eq. 3"
+    # the whole co-attention pipeline against the oracle's, head by head
+    K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
+    G = p_co.group
+    for h in range(p_co.n_heads_kv):
+        ch = O.compress_head(K64[0, h], V64[0, h], Q64[0, h * G:(h + 1) * G], window=w.window, route_mode="coattn")
+        A = O.window_attention_group(Q64[0, h * G:(h + 1) * G], K64[0, h], oracle_scale(p_co))
+        gpu = {k: (np64(v[0, h]) if v.is_floating_point() else v[0, h].cpu().numpy()) for k, v in co.items()}
+        gpu = dict(attn=gpu["attn"], score=gpu["score"], kept=gpu["kept"], evicted=gpu["evicted"],
+                   target=gpu["target"], gate=gpu["gate"], v_out=gpu["V_out"], bias=gpu["bias"], K_out=gpu["K_out"])
+        counts = compare_end_to_end(gpu, ch, K64[0, h], w.seq_len, Bk, TOL[w.dtype], float(np.float32(p_co.alpha)),
+                                    route_key=lambda j, i, A=A: float(A[:, i] @ A[:, j]))
+        record("coattn_end_to_end", f"llama_layer n=4096 h{h}", **counts)
 
 
 # ------------------------------------------------------------------ fused merge + bias (steps 3 - 6 in one pass)
@@ -1070,7 +1034,9 @@ FUSED = [
 def test_merge_bias_fused_equals_merge_then_bias(S, case):
     """selkv_merge_bias gives bit for bit what selkv_merge followed by
     selkv_bias gives, in every routing, gate, key and selection mode: the
-    bias kernels sum a slot's absorbed mass in the merge kernels' order."""
+    bias kernels sum a slot's absorbed mass in the merge kernels' order.
+    The fused outputs are then checked against the oracle's whole pipeline
+    in the same mode (near-ties of selection and routing counted)."""
     case = dict(case)
     kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
     t = synth.random_case(case["n"] * 7 + 5, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
@@ -1092,23 +1058,38 @@ def test_merge_bias_fused_equals_merge_then_bias(S, case):
         a, b = sep[k], fused[k]
         assert torch.equal(a.view(torch.int32) if a.is_floating_point() and a.element_size() == 4 else a,
                            b.view(torch.int32) if b.is_floating_point() and b.element_size() == 4 else b), k
-    # and the bias is the oracle's for every head whose kept set and targets match it
+    # and the fused outputs against the oracle's whole pipeline in the same mode
     K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
-    if kw.get("select_mode") == "union" or kw.get("route_mode") in ("coattn", "full_cosine"):
-        return   # covered against the oracle by their own stage-wise tests
     alpha = float(np.float32(p.alpha))
+    tol = TOL[case["dtype"]]
+    G, B = case["G"], p.bucket
+    if kw.get("select_mode") == "union":
+        for b in range(case["batch"]):
+            record("fused_vs_oracle", f"{case} {kw} b{b}", **union_oracle_compare(S, p, comp, K64, V64, Q64, b, tol))
+        return
+    route = {S.ROUTE_BUCKET: "bucket", S.ROUTE_FULL_COSINE: "full_cosine", S.ROUTE_BUCKET_NEAREST: "bucket_nearest",
+             S.ROUTE_COATTN: "coattn"}[p.route_mode]
     for b in range(case["batch"]):
         for h in range(case["H"]):
-            ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * case["G"]:(h + 1) * case["G"]],
-                                 window=case["W"], budget_ratio=p.budget_ratio, bucket=p.bucket,
-                                 gate_mode=GATE[p.gate_mode],
-                                 route_mode="bucket_nearest" if p.route_mode == S.ROUTE_BUCKET_NEAREST else "bucket")
-            if not np.array_equal(fused["kept"][b, h].cpu().numpy(), ch["kept"]):
-                continue
-            if not np.array_equal(fused["target"][b, h].cpu().numpy(), ch["target"]):
-                continue
-            got = np64(fused["bias"][b, h])
-            assert np.abs(got - ch["bias"]).max() <= abs(alpha) * TOL[case["dtype"]], (b, h)
+            ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * G:(h + 1) * G], window=case["W"],
+                                 budget_ratio=p.budget_ratio, bucket=B, gate_mode=GATE[p.gate_mode], route_mode=route)
+            if p.merge_keys:    # the merged-keys reading: keys take the Eq. 5 weights
+                ch["k_out"], _, _ = O.merge(K64[b, h], V64[b, h], ch["attn"], ch["kept"], ch["evicted"],
+                                            ch["target"], ch["gate"], merge_keys=True)
+            if route == "coattn":
+                A = O.window_attention_group(Q64[b, h * G:(h + 1) * G], K64[b, h], oracle_scale(p))
+                key = lambda j, i, A=A: float(A[:, i] @ A[:, j])
+            elif route == "full_cosine":
+                vv = V64[b, h]
+                nrm = np.linalg.norm(vv, axis=1)
+                key = lambda j, i, vv=vv, nrm=nrm: (0.0 if nrm[i] == 0 or nrm[j] == 0
+                                                    else float(vv[i] @ vv[j]) / (nrm[i] * nrm[j]))
+            else:
+                key = None
+            counts = compare_end_to_end(gpu_head(comp, b, h), ch, K64[b, h], case["n"], B, tol, alpha,
+                                        route_key=key, local=route in ("bucket", "coattn"),
+                                        keys_merged=bool(p.merge_keys))
+            record("fused_vs_oracle", f"{case} {kw} b{b} h{h}", **counts)
 
 
 # ------------------------------------------------------------------ selection: the threshold's top-12-bit bin
@@ -1207,8 +1188,8 @@ def test_full_cosine_full_size_sampled(S):
     attn / vnorm / kept / evicted feed the full-cosine merge call; for 512
     sampled evicted rows of two heads the float64 cosine argmax over all
     kept rows (lowest slot on ties) must be the GPU's target, except where
-    the two cosines lie within 4e-6 of each other; gates follow the chosen
-    target's cosine."""
+    the two cosines lie within 1e-6 of each other relative (counted); gates
+    follow the chosen target's cosine."""
     w = synth.WORKLOADS["ctx100k"]
     t = synth.make_layer(w, 0, DEV)
     K, V, Q = t["K"], t["V"], t["Qwin"]
@@ -1237,10 +1218,10 @@ def test_full_cosine_full_size_sampled(S):
         for r in range(len(rows)):
             c_ref, c_got = cos[r, ref[r]], cos[r, got[r]]
             if got[r] != ref[r]:
-                assert c_got >= c_ref - 4e-6 * abs(c_ref), f"head {h} row {ev[rows[r]]}: {c_got!r} vs {c_ref!r}"
+                assert c_got >= c_ref - NEAR_TIE * abs(c_ref), f"head {h} row {ev[rows[r]]}: {c_got!r} vs {c_ref!r}"
                 ties += 1
-            assert abs(g[r] - min(1.0, max(0.0, c_got))) <= TOL["bf16"], f"gate head {h} row {ev[rows[r]]}"
-    print(f"a9 full size: {ties} near-tie routing differences in 1024 sampled rows")
+            assert abs(g[r] - min(1.0, max(0.0, c_got))) <= GATE_ATOL, f"gate head {h} row {ev[rows[r]]}"
+    record("full_cosine_full_size_sampled", "ctx100k layer 0 heads 0,5 (1024 rows)", route_ties=ties)
 
 
 # ------------------------------------------------------------------ co-attention routing at the full ctx100k size, sampled
@@ -1250,7 +1231,7 @@ def test_coattn_full_size_sampled(S):
     GPU; for 512 sampled evicted tokens of two heads the float64 argmax over
     the kept tokens of the token's bucket of sum_r A[r, j] A[r, i] (A over
     all 4 x 32 window rows, lowest position on ties) must be the GPU's
-    target, except within 1e-4 relative of each other; -1 exactly where the
+    target, except within 1e-6 relative of each other; -1 exactly where the
     bucket keeps nothing; gates follow the chosen target's value cosine."""
     w = synth.WORKLOADS["ctx100k"]
     t = synth.make_layer(w, 0, DEV)
@@ -1285,12 +1266,12 @@ def test_coattn_full_size_sampled(S):
             assert tg[r] in cand, f"head {h} evicted {j}: target {tg[r]} outside its bucket"
             if tg[r] != ref:
                 c_got = float(A[:, kept[tg[r]]] @ A[:, j])
-                assert abs(c_got - co.max()) <= COATTN_NEAR_TIE * abs(co.max()), f"head {h} evicted {j}"
+                assert abs(c_got - co.max()) <= NEAR_TIE * abs(co.max()), f"head {h} evicted {j}"
                 ties += 1
             g_ref = O.gate(V64, kept, ev[r:r + 1], tg[r:r + 1], GATE[p.gate_mode], float(np.float32(p.gate_threshold)),
                            float(np.float32(p.gate_temperature)))[0]
-            assert abs(g[r] - g_ref) <= TOL["bf16"], f"gate head {h} evicted {j}"
-    print(f"co-attention full size: {ties} near-tie differences, {unrouted} unrouted in 1024 sampled rows")
+            assert abs(g[r] - g_ref) <= GATE_ATOL, f"gate head {h} evicted {j}"
+    record("coattn_full_size_sampled", "ctx100k layer 0 heads 2,7 (1024 rows)", route_ties=ties, unrouted=unrouted)
 
 
 # ------------------------------------------------------------------ decode over long, ragged and many-head caches
