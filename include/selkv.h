@@ -51,7 +51,10 @@
 extern "C" {
 #endif
 
-#define SELKV_ABI_VERSION 5
+#define SELKV_ABI_VERSION 6
+
+/* Bytes of the fixed per-GPU scratch of selkv_decode_attn_noalloc (16 MiB). */
+#define SELKV_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 typedef enum selkv_status {
   SELKV_OK = 0,
@@ -332,6 +335,26 @@ SELKV_API selkv_status selkv_rope_reposition(const selkv_params* p, const int32_
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream);
+
+/* selkv_decode_attn without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, kernels and
+ * result as selkv_decode_attn; the split partials live in a fixed scratch
+ * array of SELKV_NOALLOC_SCRATCH_BYTES that the library holds on each GPU
+ * it runs on until the process ends.  The call allocates nothing: the
+ * scratch address is looked up (hipGetSymbolAddress) on the first call on a
+ * device, with that device current; the stream must belong to the current
+ * device.  Every call on a GPU shares that GPU's scratch, so calls that may
+ * overlap in time on one GPU (different streams, other threads) race and
+ * must be serialised by the caller; the scratch needs no clearing between
+ * calls.  Returns SELKV_EWORKSPACE when the shape's split partials exceed
+ * the scratch (never while selkv_workspace_size(p, SELKV_CALL_DECODE,
+ * cache_len) is within SELKV_NOALLOC_SCRATCH_BYTES: at most 256 KV heads of
+ * any cache length, or about 4000 with G = 8 and d = 128), SELKV_EHIP if
+ * the scratch address cannot be obtained. */
+SELKV_API selkv_status selkv_decode_attn_noalloc(const selkv_params* p, const void* q, const void* K,
+                                                 const void* V, const float* bias, int32_t cache_len, float* out,
+                                                 hipStream_t stream);
 
 /* One generation step over a cache that grows (the decode loop after
  * compression, Sec. 4.4): the step attends over the cache_len + 1 entries

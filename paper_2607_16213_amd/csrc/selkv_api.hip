@@ -3,10 +3,18 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "internal.hpp"
 #include "selkv.h"
 
 using namespace selkv;
+
+// Fixed scratch of selkv_decode_attn_noalloc: one copy per GPU, held until
+// the process ends.  Host code never passes this name to a kernel (on the
+// host it is only a stand-in for the symbol); it uses the device address
+// that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[SELKV_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -84,6 +92,43 @@ size_t bias_base_bytes(const selkv_params* p, const Shape& s) { return merge_byt
 size_t bias_bytes(const selkv_params* p, const Shape& s) {
   const size_t base = bias_base_bytes(p, s);
   return is_union(p) ? round256(base) + plan_union(s).ratio_bytes : base;
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+selkv_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SELKV_EHIP;
+  if (dev >= kMaxDevices) return SELKV_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return SELKV_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return SELKV_OK;
+}
+
+// Arguments of selkv_decode_attn and selkv_decode_attn_noalloc.
+selkv_status check_decode_args(const selkv_params* p, const void* q, const void* K, const void* V, const float* bias,
+                               int32_t cache_len, float* out) {
+  if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
+  if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
+  if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || cache_len < 1) return SELKV_EINVAL;
+  if (p->group > 8) return SELKV_EUNSUPPORTED;
+  if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
+  if (!(p->scale >= 0.f) || !isfinite(p->scale)) return SELKV_EINVAL;
+  const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
+  if (heads > 65535) return SELKV_EUNSUPPORTED;
+  if (!q || !K || !V || !out) return SELKV_EINVAL;
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(bias, 4) || !aligned(out, 16))
+    return SELKV_EALIGN;
+  return SELKV_OK;
 }
 
 selkv_status check_ws(void* ws, size_t ws_bytes, size_t need) {
@@ -345,19 +390,26 @@ SELKV_API selkv_status selkv_rope_reposition(const selkv_params* p, const int32_
 SELKV_API selkv_status selkv_decode_attn(const selkv_params* p, const void* q, const void* K, const void* V,
                                          const float* bias, int32_t cache_len, float* out, void* ws,
                                          size_t ws_bytes, hipStream_t stream) {
-  if (!p || p->struct_size != sizeof(selkv_params)) return SELKV_EINVAL;
-  if (p->kv_dtype != SELKV_F32 && p->kv_dtype != SELKV_BF16) return SELKV_EDTYPE;
-  if (p->batch < 1 || p->n_heads_kv < 1 || p->group < 1 || cache_len < 1) return SELKV_EINVAL;
-  if (p->group > 8) return SELKV_EUNSUPPORTED;
-  if (p->head_dim != 64 && p->head_dim != 128) return SELKV_EUNSUPPORTED;
-  if (!(p->scale >= 0.f) || !isfinite(p->scale)) return SELKV_EINVAL;
+  selkv_status st = check_decode_args(p, q, K, V, bias, cache_len, out);
+  if (st != SELKV_OK) return st;
   const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
-  if (heads > 65535) return SELKV_EUNSUPPORTED;
-  if (!q || !K || !V || !out) return SELKV_EINVAL;
-  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(bias, 4) || !aligned(out, 16))
-    return SELKV_EALIGN;
   const DecodePlan plan = plan_decode(heads, cache_len, p->head_dim, p->group);
-  selkv_status st = check_ws(ws, ws_bytes, plan.bytes);
+  st = check_ws(ws, ws_bytes, plan.bytes);
+  if (st != SELKV_OK) return st;
+  return hip_status(launch_decode(heads, p->n_heads_kv, cache_len, cache_len, p->head_dim, p->group, p->kv_dtype,
+                                  eff_scale(p), plan, q, K, V, bias, out, ws, stream));
+}
+
+SELKV_API selkv_status selkv_decode_attn_noalloc(const selkv_params* p, const void* q, const void* K, const void* V,
+                                                 const float* bias, int32_t cache_len, float* out,
+                                                 hipStream_t stream) {
+  selkv_status st = check_decode_args(p, q, K, V, bias, cache_len, out);
+  if (st != SELKV_OK) return st;
+  const int64_t heads = (int64_t)p->batch * p->n_heads_kv;
+  const DecodePlan plan = plan_decode(heads, cache_len, p->head_dim, p->group);
+  if (plan.bytes > (size_t)SELKV_NOALLOC_SCRATCH_BYTES) return SELKV_EWORKSPACE;
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
   if (st != SELKV_OK) return st;
   return hip_status(launch_decode(heads, p->n_heads_kv, cache_len, cache_len, p->head_dim, p->group, p->kv_dtype,
                                   eff_scale(p), plan, q, K, V, bias, out, ws, stream));

@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 GATE_COSINE, GATE_DROP, GATE_MERGE_ALL = 0, 1, 2
 ROUTE_BUCKET, ROUTE_FULL_COSINE, ROUTE_BUCKET_NEAREST, ROUTE_COATTN = 0, 1, 2, 3
 SELECT_PER_HEAD, SELECT_UNION = 0, 1
-ABI_VERSION = 5
+ABI_VERSION = 6
 CALL_SCORE, CALL_SELECT, CALL_MERGE, CALL_BIAS, CALL_DECODE, CALL_ROUTE, CALL_MERGE_BIAS = range(7)
 STATUS = {0: "SELKV_OK", 1: "SELKV_EINVAL", 2: "SELKV_EDTYPE", 3: "SELKV_EUNSUPPORTED", 4: "SELKV_EALIGN",
           5: "SELKV_EWORKSPACE", 6: "SELKV_EHIP"}
@@ -78,6 +78,7 @@ def _load():
         "selkv_bias": (ctypes.c_int, [P, fp, ip, ip, ip, fp, fp, vp, sz, vp]),
         "selkv_merge_bias": (ctypes.c_int, [P, vp, vp, fp, fp, ip, ip, vp, vp, ip, fp, fp, vp, sz, vp]),
         "selkv_decode_attn": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp, sz, vp]),
+        "selkv_decode_attn_noalloc": (ctypes.c_int, [P, vp, vp, vp, fp, i32, fp, vp]),
         "selkv_rope_reposition": (ctypes.c_int, [P, ip, vp, ctypes.c_double, vp]),
         "selkv_decode_append": (ctypes.c_int, [P, vp, vp, vp, vp, vp, fp, i32, i32, fp, vp, sz, vp]),
         "selkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -268,6 +269,21 @@ def decode_attn(p, q, K, V, bias_in, out, ws, stream=None):
     _dev(out, (B, H * p.group, d), torch.float32, "out")
     _check(lib.selkv_decode_attn(ctypes.byref(p), _ptr(q), _ptr(K), _ptr(V), _ptr(bias_in), L, _ptr(out), _ptr(ws),
                                  _nbytes(ws), _stream(stream)), "selkv_decode_attn")
+
+
+def decode_attn_noalloc(p, q, K, V, bias_in, out, stream=None):
+    """selkv_decode_attn with the library's fixed per-GPU scratch instead of a
+    workspace (nothing is allocated; calls overlapping on one GPU race)."""
+    B, H, d = p.batch, p.n_heads_kv, p.head_dim
+    L = K.shape[2]
+    dt = _kvdt(p)
+    _dev(q, (B, H * p.group, d), dt, "q")
+    _dev(K, (B, H, L, d), dt, "K"); _dev(V, (B, H, L, d), dt, "V")
+    if bias_in is not None:
+        _dev(bias_in, (B, H, L), torch.float32, "bias")
+    _dev(out, (B, H * p.group, d), torch.float32, "out")
+    _check(lib.selkv_decode_attn_noalloc(ctypes.byref(p), _ptr(q), _ptr(K), _ptr(V), _ptr(bias_in), L, _ptr(out),
+                                         _stream(stream)), "selkv_decode_attn_noalloc")
 
 
 def decode_append(p, q, k_new, v_new, K, V, bias_io, cache_len, out, ws, stream=None):

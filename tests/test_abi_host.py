@@ -63,7 +63,7 @@ def test_params_init_defaults(S):
     assert p.struct_size == ctypes.sizeof(S.Params)
     assert (p.window, p.pool_kernel, p.recent, p.bucket) == (32, 5, 16, 32)
     assert abs(p.alpha - 0.5) < 1e-7 and p.budget_ratio == 0.25
-    assert S.lib.selkv_abi_version() == 5
+    assert S.lib.selkv_abi_version() == 6
     assert S.lib.selkv_status_string(0) == b"success"
 
 
