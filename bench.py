@@ -54,6 +54,7 @@ def parse():
                     help="skip the all-layers-in-one-call decode timing (profiles of the per-layer call)")
     ap.add_argument("--no-union", action="store_true",
                     help="skip the timings of the alternative modes (GQA union, nearest-kept fallback, merged keys)")
+    ap.add_argument("--no-mha", action="store_true", help="skip the MHA workload (budget and gate sweep) point")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration for profiling passes)")
     return ap.parse_args()
@@ -199,9 +200,37 @@ def stage_bytes(w, m):
     return dict(score=score, select=select, merge_bias=merge_bias), per_decode, full_decode
 
 
-def cpu_baseline(job, n_heads, dev):
+def _oracle_slice(args):
+    """Worker of the multi-core oracle timing: one (layer, KV head) slice
+    given as raw bf16 / fp32 storage, upcast exactly, compressed by the
+    float64 oracle.  Returns the seconds it took."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import selkv_oracle as O
+    K, V, Q, bf16, window, rho = args
+    up = (lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)) if bf16 else \
+        (lambda a: a.astype(np.float64))
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        O.compress_head(up(K), up(V), up(Q), window=window, budget_ratio=rho)
+        return time.perf_counter() - t0
+
+
+def _raw(t):
+    """Storage bits of a device tensor as numpy (bf16 as uint16)."""
+    import torch
+    t = t.detach().contiguous().cpu()
+    return t.view(torch.int16).numpy().view("uint16") if t.dtype == torch.bfloat16 else t.numpy()
+
+
+def cpu_baseline(job, n_heads, dev, extra_jobs=()):
     """The float64 oracle, as it stands, on sampled (layer, head) slices of
-    the same workload, single-threaded; scaled to the whole job."""
+    the same workload: once single-threaded in this process, and once with
+    the slices spread over the host's cores (one process per core, BLAS one
+    thread each); scaled to the whole job.  The single-threaded pass also
+    gives the slices compared with the GPU's outputs (parity_sample)."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
     import numpy as np
     from threadpoolctl import threadpool_limits
     from oracle import selkv_oracle as O
@@ -218,7 +247,6 @@ def cpu_baseline(job, n_heads, dev):
             r = O.compress_head(K, V, Q, window=w.window, budget_ratio=w.budgets[0])
             t_comp += time.perf_counter() - t0
             outs.append((layer, h, r))
-    job.oracle_outs = outs      # compared with the GPU's outputs by parity_sample()
     with threadpool_limits(1):
         t_dec, nd = 0.0, 0
         for (layer, h, r) in outs:
@@ -228,54 +256,203 @@ def cpu_baseline(job, n_heads, dev):
                 O.decode(q, r["k_out"][None], r["v_out"][None], r["bias"][None], w.group, 1 / math.sqrt(w.head_dim))
                 t_dec += time.perf_counter() - t0
                 nd += 1
+    # the same slices over the host cores: the machine's CPU share, at most 16 processes
+    cores = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()))
+    work = [(_raw(job.K[layer, 0, h]), _raw(job.V[layer, 0, h]),
+             _raw(job.Q[layer, 0, h * w.group:(h + 1) * w.group]), w.dtype == "bf16", w.window, w.budgets[0])
+            for (layer, h) in picks]
+    t0 = time.perf_counter()
+    with cf.ProcessPoolExecutor(max_workers=cores, mp_context=mp.get_context("spawn")) as ex:
+        list(ex.map(_oracle_slice, work))
+    wall_multi = time.perf_counter() - t0
+    del work
     per_head = t_comp / len(picks)
     heads_total = w.layers * w.batch * w.n_heads_kv
+    tok = w.seq_len * w.batch          # tokens of the whole job (every layer and KV head of them)
+    samples = {w.name: parity_sample(job, outs)}
+    for j in extra_jobs:
+        samples[j.w.name] = parity_sample(j, None)
     return {
-        "value": w.seq_len * w.batch / (per_head * heads_total),
+        "value": tok / (wall_multi / len(picks) * heads_total),
         "unit": "tokens/s",
-        "cores": 1,
+        "cores": cores,
         "kind": "oracle",
         "sample": f"float64 oracle compress_head on {len(picks)} (layer, KV head) slices of {w.name} "
-                  f"(n={w.seq_len}), scaled to {heads_total} slices; decode on {nd} (slice, step) samples",
-        "seconds": round(t_comp + t_dec, 2),
+                  f"(n={w.seq_len}) spread over {cores} processes (wall clock incl. process start), scaled to "
+                  f"{heads_total} slices; decode on {nd} (slice, step) samples, one thread",
+        "value_1thread": tok / (per_head * heads_total),
+        "seconds": round(t_comp + t_dec + wall_multi, 2),
         "decode_us_per_layer_step": 1e6 * (t_dec / nd) * w.n_heads_kv,
-        "parity_sample": parity_sample(job),
+        "parity_sample": samples,
     }
 
 
-def parity_sample(job):
-    """The GPU's default compression of the whole job against the oracle on
-    the slices cpu_baseline() sampled: the largest relative score and
-    attention errors, and how many slices keep exactly the oracle's set.
-    The parity tests accept selection swaps only between scores closer than
-    max(1e-6, 4 x the score error); score_err_above_1e-6 says when that band
-    is wider than 1e-6."""
+NEAR_TIE = 1e-6   # relative score gap within which two choices count as tied
+
+
+def _slice_parity(c, i, h, r):
+    """One (batch row, KV head) slice of the GPU's compression against the
+    oracle's compress_head() result r: relative score / attention errors,
+    kept positions that differ (near-ties within NEAR_TIE of the selection
+    threshold, or beyond it), and evicted tokens routed differently (ties
+    whose window attentions lie within NEAR_TIE, or beyond)."""
     import numpy as np
-    torch = job.torch
+    s = c.score[i, h].double().cpu().numpy()
+    a = c.attn[i, h].double().cpu().numpy()
+    es = float((np.abs(s - r["score"]) / np.maximum(np.abs(r["score"]), 1e-30)).max(initial=0.0))
+    ea = float((np.abs(a - r["attn"]) / np.maximum(np.abs(r["attn"]), 1e-30)).max(initial=0.0))
+    kept = c.kept[i, h].cpu().numpy()
+    ms = r["ms"]
+    thr = np.sort(r["score"])[::-1][ms - 1] if ms > 0 else 0.0
+    diff = set(kept.tolist()) ^ set(r["kept"].tolist())
+    near = sum(1 for j in diff if abs(r["score"][j] - thr) <= NEAR_TIE * abs(thr))
+    out = dict(score_rel_err=es, attn_rel_err=ea, kept_equal=not diff, near_tie_positions=near,
+               out_of_band_positions=len(diff) - near, route_ties=0, route_beyond_band=0)
+    if not diff:          # routing by position on equal kept sets
+        ev = c.evicted[i, h].cpu().numpy()
+        tg = c.target[i, h].cpu().numpy()
+        pg = np.where(tg >= 0, kept[np.maximum(tg, 0)], -1)
+        pr = np.where(r["target"] >= 0, r["kept"][np.maximum(r["target"], 0)], -1)
+        for e in np.flatnonzero((pg != pr) & (ev == r["evicted"])):
+            a1, a2 = (r["attn"][pg[e]], r["attn"][pr[e]]) if pg[e] >= 0 and pr[e] >= 0 else (0.0, 1.0)
+            if abs(a1 - a2) <= NEAR_TIE * max(a1, a2):
+                out["route_ties"] += 1
+            else:
+                out["route_beyond_band"] += 1
+    return out
+
+
+def parity_sample(job, outs=None, max_slices=8):
+    """The GPU's default compression of a job against the float64 oracle on
+    sampled slices (those cpu_baseline() timed, or up to max_slices spread
+    over the job's layers and heads): the largest relative score and
+    attention errors and the near-tie counts (selection and routing) at the
+    fixed 1e-6 band."""
+    import numpy as np
+    from oracle import selkv_oracle as O
+    torch, w = job.torch, job.w
     job.compress()
     torch.cuda.synchronize()
-    c, B = job.comp, job.w.batch
-    es, ea, same, ties_only = 0.0, 0.0, 0, 0
-    diffs = []
-    for (layer, h, r) in job.oracle_outs:
-        i = layer * B
-        s = c.score[i, h].double().cpu().numpy()
-        a = c.attn[i, h].double().cpu().numpy()
-        es = max(es, float((np.abs(s - r["score"]) / np.maximum(np.abs(r["score"]), 1e-30)).max(initial=0.0)))
-        ea = max(ea, float((np.abs(a - r["attn"]) / np.maximum(np.abs(r["attn"]), 1e-30)).max(initial=0.0)))
-        kept = c.kept[i, h].cpu().numpy()
-        if np.array_equal(kept, r["kept"]):
-            same += 1
-        else:
-            diffs.append((set(kept.tolist()) ^ set(r["kept"].tolist()), r))
-    band = max(1e-6, 4 * es)
-    for (d, r) in diffs:   # every differing position within the band of the selection threshold?
-        ms = r["ms"]
-        thr = np.sort(r["score"])[::-1][ms - 1]
-        ties_only += int(all(abs(r["score"][j] - thr) <= band * abs(thr) for j in d))
-    return {"slices": len(job.oracle_outs), "score_rel_err_max": es, "attn_rel_err_max": ea,
-            "kept_equal_slices": same, "kept_differ_by_near_ties_only": ties_only,
-            "near_tie_band": band, "score_err_above_1e-6": bool(es > 1e-6)}
+    c, B = job.comp, w.batch
+    if outs is None:
+        f64 = lambda x: x.detach().double().cpu().numpy()
+        picks = [(li, h) for li in range(w.layers) for h in range(w.n_heads_kv)]
+        if len(picks) > max_slices:
+            rng = np.random.default_rng(1607)
+            picks = [picks[k] for k in sorted(rng.choice(len(picks), max_slices, replace=False))]
+        outs = []
+        for (li, h) in picks:
+            r = O.compress_head(f64(job.K[li, 0, h]), f64(job.V[li, 0, h]),
+                                f64(job.Q[li, 0, h * w.group:(h + 1) * w.group]), window=w.window,
+                                budget_ratio=w.budgets[0])
+            outs.append((li, h, r))
+    per = [_slice_parity(c, layer * B, h, r) for (layer, h, r) in outs]
+    agg = {"slices": len(per), "score_rel_err_max": max(x["score_rel_err"] for x in per),
+           "attn_rel_err_max": max(x["attn_rel_err"] for x in per),
+           "kept_equal_slices": sum(x["kept_equal"] for x in per)}
+    for k in ("near_tie_positions", "out_of_band_positions", "route_ties", "route_beyond_band"):
+        agg[k] = sum(x[k] for x in per)
+    agg["near_tie_band"] = NEAR_TIE
+    agg["score_err_above_1e-6"] = bool(agg["score_rel_err_max"] > NEAR_TIE)
+    return agg
+
+
+def measure_copy_ceiling(dev, reps=10):
+    """torch's device copy of 1 GiB into another 1 GiB (read + write), the
+    measured copy-kernel rate the stage fractions are also quoted against."""
+    import torch
+    src = torch.ones((1 << 30) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del src, dst
+    return round(2 * (1 << 30) / (us * 1e-6) / 1e9, 1)
+
+
+def measure_mha(dev, reps=5, decode_steps=128):
+    """The MHA workload (batch 4 x 32 heads = 32 KV heads, G = 1, n = 16384,
+    W = 64): compress tokens/s at each budget with the paper's gate, the
+    fused merge + bias time over the nine (tau, T) gate settings, and the
+    128-step decode over each budget's compressed caches (HIP graph)."""
+    import torch
+    from paper_2607_16213_amd import selkv, synth
+    w = synth.WORKLOADS["mha_sweep"]
+    t = synth.make_layer(w, 0, dev)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    qd = synth.make_decode_queries(w, 0, decode_steps, dev)
+    out = {}
+    for rho in w.budgets:
+        p = selkv.params(batch=w.batch, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim,
+                         seq_len=w.seq_len, window=w.window, kv_dtype=w.dtype, budget_ratio=rho)
+        comp = selkv.Compressor(p, dev)
+        comp.run(K, V, Q)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            comp.run(K, V, Q)
+        e[1].record()
+        torch.cuda.synchronize()
+        ms = e[0].elapsed_time(e[1]) / reps
+        mb = []
+        for (tau, T) in w.gate_sweep:
+            pg = selkv.params(batch=w.batch, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim,
+                              seq_len=w.seq_len, window=w.window, kv_dtype=w.dtype, budget_ratio=rho,
+                              gate_threshold=tau, gate_temperature=T)
+            args = (pg, K, V, comp.attn, comp.vnorm, comp.kept, comp.evicted, comp.K_out, comp.V_out, comp.target,
+                    comp.gate, comp.bias, comp.ws_merge)
+            selkv.merge_bias(*args)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            selkv.merge_bias(*args)
+            e1.record()
+            torch.cuda.synchronize()
+            mb.append(e0.elapsed_time(e1))
+        comp.run(K, V, Q)          # the paper's gate for the decode cache
+        pd = selkv.params(batch=w.batch, n_heads_kv=w.n_heads_kv, group=w.group, head_dim=w.head_dim,
+                          kv_dtype=w.dtype)
+        dec = selkv.Decoder(pd, comp.m, dev)
+        outs = torch.empty((decode_steps,) + tuple(dec.out.shape), dtype=torch.float32, device=dev)
+
+        def loop():
+            for s in range(decode_steps):
+                dec.run(qd[s], comp.K_out, comp.V_out, comp.bias, out=outs[s])
+        loop()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            loop()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            loop()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        dus = e0.elapsed_time(e1) * 1e3 / decode_steps
+        el = 2
+        dbytes = w.batch * w.n_heads_kv * (2 * comp.m * w.head_dim * el + 4 * comp.m) + \
+            w.batch * w.n_heads_q * w.head_dim * (el + 4)
+        out[str(rho)] = {"retained_per_head": comp.m, "compress_ms": round(ms, 4),
+                         "compress_tokens_per_s": round(w.seq_len * w.batch / (ms * 1e-3), 1),
+                         "merge_bias_ms_over_gate_sweep": [round(min(mb), 4), round(max(mb), 4)],
+                         "decode_us_per_step": round(dus, 3),
+                         "decode_GBs": round(dbytes / (dus * 1e-6) / 1e9, 1)}
+        del comp, dec, outs, g
+    return out
 
 
 def measure(job, steps, warmup):
@@ -537,13 +714,15 @@ def main():
     dec_us = st["decode"] * 1e3 / n_dec
     decode_gbs = per_decode / (dec_us * 1e-6) / 1e9
 
+    copy_gbs = measure_copy_ceiling(dev)
     stages = {}
     for k in STAGES:
         gbs = sb[k] / (st[k] * 1e-3) / 1e9
         stages[k] = {"ms": round(st[k], 4), "alg_bytes": sb[k], "achieved_GBs": round(gbs, 1),
-                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "frac_copy": round(gbs / copy_gbs, 4)}
     stages["decode"] = {"us_per_launch": round(dec_us, 3), "alg_bytes_per_launch": per_decode,
-                        "achieved_GBs": round(decode_gbs, 1), "frac_hbm": round(decode_gbs / HBM_PEAK_GBS, 4)}
+                        "achieved_GBs": round(decode_gbs, 1), "frac_hbm": round(decode_gbs / HBM_PEAK_GBS, 4),
+                        "frac_copy": round(decode_gbs / copy_gbs, 4)}
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(wall * 1e3, 3), "higher_is_better": True, "scaling": "weak",
@@ -553,6 +732,7 @@ def main():
                       "budget_ratio": w.budgets[0], "decode_steps": T, "retained_per_kv_head": job.m,
                       "decode_launch": "hip_graph" if job.graph is not None else "eager"},
            "compress_ms": round(comp_ms, 4),
+           "copy_ceiling_GBs": copy_gbs,
            "decode_us_per_layer_step": round(dec_us, 3),
            "decode_us_per_token": round(dec_us * w.layers, 2),
            "stages": stages}
@@ -584,9 +764,11 @@ def main():
         out["rope_reposition"] = measure_rope(job)
 
     traffic = read_traffic()
-    out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm", "achieved": round(decode_gbs, 1),
-                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_gbs / HBM_PEAK_GBS, 4),
-                       "traffic": traffic, "alg_bytes_per_launch": per_decode}
+    out["roofline"] = {"kernel": "selkv_decode_attn (decode_mfma_kernel + decode_reduce_kernel)", "bound": "hbm",
+                       "achieved": round(decode_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": round(decode_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                       "alg_bytes_per_launch": per_decode, "copy_ceiling_GBs": copy_gbs,
+                       "frac_copy_ceiling": round(decode_gbs / copy_gbs, 4)}
 
     if args.copy_calibration:
         # a plain elementwise kernel that reads 1 GiB and writes 1 GiB, to
@@ -597,6 +779,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    extra = []
     if not args.no_32k and w.name != "ctx32k":
         w32 = synth.WORKLOADS["ctx32k"]
         j32 = Job(w32, dev, w32.decode_steps if args.decode_steps is None else min(args.decode_steps, w32.decode_steps),
@@ -613,9 +796,13 @@ def main():
                          "decode_GBs": round(pd32 / (d32 * 1e-6) / 1e9, 1),
                          "score_GBs": round(sb32["score"] / (st32["score"] * 1e-3) / 1e9, 1),
                          "merge_bias_GBs": round(sb32["merge_bias"] / (st32["merge_bias"] * 1e-3) / 1e9, 1)}
-        del j32
+        extra.append(j32)
+    if not args.no_mha:
+        out["mha_sweep"] = measure_mha(dev)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(job, args.cpu_heads, dev)
+        # the parity sample also covers the small workloads (whole layers)
+        extra += [Job(synth.WORKLOADS[name], dev, 1, False, False) for name in ("llama_layer", "tiny")]
+        out["cpu_baseline"] = cpu_baseline(job, args.cpu_heads, dev, extra)
     print(json.dumps(out), flush=True)
 
 
