@@ -7,10 +7,11 @@
 //            running argmax per evicted row (lowest kept slot on ties), then
 //            the gate of Sec. 3.5 from the best cosine.  The |E| x |S| matrix
 //            is never written.
-//   group    a stable grouping of the evicted tokens by target slot:
-//            integer-atomic counts, an exclusive scan, and one wave per head
-//            scattering the tokens in ascending order (ranks among equal
-//            targets from ballots), so every slot's list is ascending.
+//   group    a stable grouping of the evicted tokens by target slot: an LSD
+//            radix sort of the target slots carrying the token index (8 bits
+//            per pass; block histograms, a scan, ballot-ranked scatter),
+//            then every slot's list offset by binary search, so every
+//            slot's list ascends.
 //   merge    one wave per kept slot: Eq. 5 over its list in a fixed order;
 //            keys gathered, values copied bit for bit when nothing is absorbed.
 //   bias     one wave per kept slot: Eq. 6 over the same lists.
@@ -408,19 +409,6 @@ __global__ __launch_bounds__(kThreads) void match_parts_kernel(MatchArgs a) {
   write_match(a, head, e, best, slot);
 }
 
-__global__ __launch_bounds__(kThreads) void fill_zero_kernel(int32_t* p, int64_t count) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i < count) p[i] = 0;
-}
-
-// cnt[head][t] += 1 for every routed evicted token (integer atomics).
-__global__ __launch_bounds__(kThreads) void group_count_kernel(const int32_t* target, int32_t* cnt, int ne, int m) {
-  const int64_t head = blockIdx.y;
-  const int e = blockIdx.x * kThreads + threadIdx.x;
-  if (e >= ne) return;
-  const int t = target[(size_t)head * ne + e];
-  if (t >= 0 && t < m) atomicAdd(cnt + (size_t)head * (m + 1) + t, 1);
-}
 
 // In place: cnt[head][0..m] becomes the exclusive prefix sum (off[m] = total).
 __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
@@ -449,59 +437,126 @@ __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
   }
 }
 
-// One wave per (head, range of kScatterSlots slots): it reads every evicted
-// token of the head in ascending order, 64 at a time, and places those whose
-// target lies in its range; each token's rank among equal targets in its
-// group of 64 comes from ballots, the write cursors live in LDS.  The targets
-// are loaded kScatterAhead groups ahead with clamped indices, and every lane
-// stores (lanes without a token into a sink), so no memory access sits
-// behind a branch and the wave never waits for its own stores.  A single
-// wave's LDS accesses stay in program order, so no barrier is needed between
-// reading a cursor and advancing it.
-constexpr int kScatterBits = 10;
-constexpr int kScatterSlots = 1 << kScatterBits;
-constexpr int kScatterAhead = 8;
+// Stable grouping of the evicted tokens by target slot as an LSD radix sort
+// of the keys (target slot, or m for a token routed nowhere) carrying the
+// token index, 8 key bits per pass.  Each pass: a digit histogram per block
+// of kSortBlock tokens (digit-major table), the exclusive scan of the table
+// per head, and a scatter in which each block ranks its tokens stably: wave
+// w takes the block's tokens w*512 .. w*512+511 in eight rounds of 64; a
+// token's rank among equal digits in its round comes from ballots, the
+// wave's running count per digit lives in LDS (a wave's LDS accesses stay in
+// program order), and the waves' counts are prefixed in wave order.  Equal
+// keys therefore keep ascending token order, so every slot's list ascends.
+// Then off[s] = the first sorted position whose key is >= s (binary search).
+constexpr int kSortWaveTok = 512;                   // tokens per wave per block
+constexpr int kSortBlock = kWaves * kSortWaveTok;   // tokens per block
+constexpr int kBins = 256;                          // 8-bit digits
 
-__global__ __launch_bounds__(64) void group_scatter_kernel(const int32_t* target, const int32_t* off, int32_t* list,
-                                                           int32_t* sink, int ne, int m) {
-  __shared__ int32_t cur[kScatterSlots];
+__device__ __forceinline__ int sort_key(const int32_t* keys_in, const int32_t* th, int e, int m) {
+  if (keys_in) return keys_in[e];
+  const int t = th[e];
+  return (t >= 0 && t < m) ? t : m;
+}
+
+// keys_in == nullptr: the first pass, keys from the targets, values = token index
+__global__ __launch_bounds__(kThreads) void sort_hist_kernel(const int32_t* keys_in, const int32_t* target,
+                                                             int32_t* table, int ne, int m, int shift, int nblk) {
+  __shared__ int hist[kBins];
   const int64_t head = blockIdx.y;
-  const int s0 = blockIdx.x * kScatterSlots;
-  const int lane = threadIdx.x;
+  const int blk = blockIdx.x, tid = threadIdx.x;
+  const int32_t* kin = keys_in ? keys_in + (size_t)head * ne : nullptr;
   const int32_t* th = target + (size_t)head * ne;
-  const int32_t* oh = off + (size_t)head * (m + 1);
-  int32_t* lh = list + (size_t)head * ne;
-  const int range = min(kScatterSlots, m - s0);
-  for (int s = lane; s < range; s += 64) cur[s] = oh[s0 + s];
+  for (int d = tid; d < kBins; d += kThreads) hist[d] = 0;
+  __syncthreads();
+  for (int k = 0; k < kSortBlock / kThreads; ++k) {
+    const int e = blk * kSortBlock + k * kThreads + tid;
+    if (e < ne) atomicAdd(&hist[(sort_key(kin, th, e, m) >> shift) & (kBins - 1)], 1);
+  }
+  __syncthreads();
+  int32_t* tab = table + (size_t)head * (kBins * nblk + 1);
+  for (int d = tid; d < kBins; d += kThreads) tab[(size_t)d * nblk + blk] = hist[d];
+}
+
+__global__ __launch_bounds__(kThreads) void sort_scatter_kernel(const int32_t* keys_in, const int32_t* vals_in,
+                                                                const int32_t* target, const int32_t* table,
+                                                                int32_t* keys_out, int32_t* vals_out, int ne, int m,
+                                                                int shift, int nblk) {
+  constexpr int R = kSortWaveTok / 64;
+  __shared__ int wcnt[kWaves][kBins];
+  const int64_t head = blockIdx.y;
+  const int blk = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int32_t* kin = keys_in ? keys_in + (size_t)head * ne : nullptr;
+  const int32_t* vin = vals_in ? vals_in + (size_t)head * ne : nullptr;
+  const int32_t* th = target + (size_t)head * ne;
+  for (int d = tid; d < kWaves * kBins; d += kThreads) wcnt[d / kBins][d % kBins] = 0;
   __syncthreads();
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const int nbatch = (ne + 63) / 64;
-  int tq[kScatterAhead];
+  int key[R], val[R], rnk[R];
+  const int base = blk * kSortBlock + wave * kSortWaveTok;
 #pragma unroll
-  for (int k = 0; k < kScatterAhead; ++k) tq[k] = th[min(k * 64 + lane, ne - 1)];
-  for (int b0 = 0; b0 < nbatch; b0 += kScatterAhead) {
+  for (int r = 0; r < R; ++r) {
+    const int e = base + r * 64 + lane;
+    const bool valid = e < ne;
+    const int ec = valid ? e : ne - 1;
+    key[r] = sort_key(kin, th, ec, m);
+    val[r] = vin ? vin[ec] : ec;
+  }
 #pragma unroll
-    for (int k = 0; k < kScatterAhead; ++k) {
-      const int e = (b0 + k) * 64 + lane;
-      const int t = (e < ne ? tq[k] : -1) - s0;            // slot relative to the range
-      tq[k] = th[min((b0 + k + kScatterAhead) * 64 + lane, ne - 1)];
-      const bool valid = t >= 0 && t < range;
-      uint64_t peers = __ballot(valid);
+  for (int r = 0; r < R; ++r) {
+    const bool valid = base + r * 64 + lane < ne;
+    const int d = (key[r] >> shift) & (kBins - 1);
+    uint64_t peers = __ballot(valid);
 #pragma unroll
-      for (int bit = 0; bit < kScatterBits; ++bit) {       // lanes with the same slot
-        const bool one = (t >> bit) & 1;
-        const uint64_t ones = __ballot(valid && one);
-        peers &= one ? ones : ~ones;
-      }
-      if (!valid) peers = 0ull;
-      const int rank = __popcll(peers & below);
-      const int start = cur[valid ? t : 0];
-      int32_t* dst = valid ? lh + start + rank : sink + lane;
-      *dst = e;
-      const bool last = valid && ((peers >> lane) >> 1) == 0ull;   // highest lane of its slot
-      if (last) cur[t] = start + rank + 1;
+    for (int bit = 0; bit < 8; ++bit) {                  // lanes holding the same digit
+      const bool one = (d >> bit) & 1;
+      const uint64_t ones = __ballot(valid && one);
+      peers &= one ? ones : ~ones;
+    }
+    if (!valid) peers = 0ull;
+    const int before = wcnt[wave][d];
+    rnk[r] = before + __popcll(peers & below);
+    const bool last = valid && ((peers >> lane) >> 1) == 0ull;    // highest lane of its digit
+    if (last) wcnt[wave][d] = before + __popcll(peers);
+  }
+  __syncthreads();
+  // per digit: the counts of the waves before each wave
+  for (int d = tid; d < kBins; d += kThreads) {
+    int run = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int c = wcnt[w][d];
+      wcnt[w][d] = run;
+      run += c;
     }
   }
+  __syncthreads();
+  const int32_t* tab = table + (size_t)head * (kBins * nblk + 1);
+  int32_t* ko = keys_out + (size_t)head * ne;
+  int32_t* vo = vals_out + (size_t)head * ne;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (base + r * 64 + lane < ne) {
+      const int d = (key[r] >> shift) & (kBins - 1);
+      const int dst = tab[(size_t)d * nblk + blk] + wcnt[wave][d] + rnk[r];
+      ko[dst] = key[r];
+      vo[dst] = val[r];
+    }
+  }
+}
+
+// off[head][s] for s = 0 .. m: the first position of the sorted keys that is >= s.
+__global__ __launch_bounds__(kThreads) void sort_offsets_kernel(const int32_t* keys, int32_t* off, int ne, int m) {
+  const int64_t head = blockIdx.y;
+  const int s = blockIdx.x * kThreads + threadIdx.x;
+  if (s > m) return;
+  const int32_t* k = keys + (size_t)head * ne;
+  int lo = 0, hi = ne;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (k[mid] < s) lo = mid + 1;
+    else hi = mid;
+  }
+  off[(size_t)head * (m + 1) + s] = lo;
 }
 
 struct GroupMergeArgs {
@@ -684,14 +739,26 @@ int match_parts(const Shape& s) {
 
 }  // namespace
 
+int sort_passes(int m) {
+  int bits = 1;
+  while ((1ll << bits) < (int64_t)m + 1) ++bits;      // keys 0 .. m
+  return (bits + 7) / 8;
+}
+
 GroupPlan plan_group(const Shape& s) {
   GroupPlan p{};
   const size_t ne = (size_t)(s.n - s.m);
+  const size_t nel = ne > 0 ? ne : 1;
+  const int nblk = (int)((nel + kSortBlock - 1) / kSortBlock);
   p.off_off = 0;
-  p.cursor_off = align256((size_t)s.heads * (s.m + 1) * sizeof(int32_t));
-  p.list_off = p.cursor_off;
-  p.sink_off = p.list_off + align256((ne > 0 ? ne : 1) * (size_t)s.heads * sizeof(int32_t));
-  p.bytes = p.sink_off + align256(64 * sizeof(int32_t));
+  p.table_off = align256((size_t)s.heads * (s.m + 1) * sizeof(int32_t));
+  p.keys_off[0] = p.table_off + align256((size_t)s.heads * ((size_t)kBins * nblk + 1) * sizeof(int32_t));
+  p.vals_off[0] = p.keys_off[0] + align256(nel * (size_t)s.heads * sizeof(int32_t));
+  p.keys_off[1] = p.vals_off[0] + align256(nel * (size_t)s.heads * sizeof(int32_t));
+  p.vals_off[1] = p.keys_off[1] + align256(nel * (size_t)s.heads * sizeof(int32_t));
+  p.bytes = p.vals_off[1] + align256(nel * (size_t)s.heads * sizeof(int32_t));
+  p.passes = sort_passes(s.m);
+  p.list_off = p.vals_off[(p.passes - 1) & 1];    // the last pass's values
   // the match's per-run results come first and are consumed before the grouping starts
   const int parts = match_parts(s);
   p.match_parts = parts;
@@ -746,19 +813,26 @@ hipError_t launch_cosine_match(const Shape& s, const GroupPlan& gp, int dtype, i
 
 hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* target, void* ws, hipStream_t st) {
   const int ne = s.n - s.m;
+  if (ne <= 0) return hipSuccess;
   char* w = static_cast<char*>(ws);
   int32_t* off = reinterpret_cast<int32_t*>(w + p.off_off);
-  int32_t* list = reinterpret_cast<int32_t*>(w + p.list_off);
-  const int64_t cnt = s.heads * (int64_t)(s.m + 1);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((cnt + kThreads - 1) / kThreads)), dim3(kThreads), 0, st, off,
-                     cnt);
-  if (ne > 0)
-    hipLaunchKernelGGL(group_count_kernel, dim3((ne + kThreads - 1) / kThreads, (unsigned)s.heads), dim3(kThreads), 0,
-                       st, target, off, ne, s.m);
-  hipLaunchKernelGGL(group_scan_kernel, dim3((unsigned)s.heads), dim3(1024), 0, st, off, s.m);
-  if (ne > 0)
-    hipLaunchKernelGGL(group_scatter_kernel, dim3((s.m + kScatterSlots - 1) / kScatterSlots, (unsigned)s.heads),
-                       dim3(64), 0, st, target, off, list, reinterpret_cast<int32_t*>(w + p.sink_off), ne, s.m);
+  int32_t* table = reinterpret_cast<int32_t*>(w + p.table_off);
+  const int nblk = (ne + kSortBlock - 1) / kSortBlock;
+  const dim3 grid((unsigned)nblk, (unsigned)s.heads);
+  const int32_t* kin = nullptr;
+  const int32_t* vin = nullptr;
+  for (int pass = 0; pass < p.passes; ++pass) {
+    int32_t* kout = reinterpret_cast<int32_t*>(w + p.keys_off[pass & 1]);
+    int32_t* vout = reinterpret_cast<int32_t*>(w + p.vals_off[pass & 1]);
+    hipLaunchKernelGGL(sort_hist_kernel, grid, dim3(kThreads), 0, st, kin, target, table, ne, s.m, 8 * pass, nblk);
+    hipLaunchKernelGGL(group_scan_kernel, dim3((unsigned)s.heads), dim3(1024), 0, st, table, kBins * nblk);
+    hipLaunchKernelGGL(sort_scatter_kernel, grid, dim3(kThreads), 0, st, kin, vin, target, table, kout, vout, ne,
+                       s.m, 8 * pass, nblk);
+    kin = kout;
+    vin = vout;
+  }
+  hipLaunchKernelGGL(sort_offsets_kernel, dim3((unsigned)((s.m + 1 + kThreads - 1) / kThreads), (unsigned)s.heads),
+                     dim3(kThreads), 0, st, kin, off, ne, s.m);
   return hipGetLastError();
 }
 

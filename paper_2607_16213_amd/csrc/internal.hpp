@@ -41,7 +41,8 @@ struct DecodePlan {
 
 // Workspace of the grouping by target slot (full-cosine routing).
 struct GroupPlan {
-  size_t off_off, cursor_off, list_off, sink_off, bytes;   // sink: stores of lanes with nothing to place
+  size_t off_off, table_off, keys_off[2], vals_off[2], list_off, bytes;   // list: the last sort pass's values
+  int passes;               // 8-bit radix passes over the keys 0 .. m
   int match_parts;          // runs the bf16 match splits the kept range into
   size_t match_slot_off;    // their per-run results: values at 0, slots at match_slot_off
 };
