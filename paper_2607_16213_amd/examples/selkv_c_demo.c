@@ -2,6 +2,9 @@
  * come from hipMalloc, and the five hot-path calls run in the paper's order
  * (Algorithm 1: score, select, merge, bias, then one biased decode step),
  * with the default parameters of selkv_params_init and fp32 storage.
+ * It also checks, in C, that the fused selkv_merge_bias equals selkv_merge
+ * + selkv_bias and that selkv_decode_attn_noalloc equals selkv_decode_attn,
+ * bit for bit.
  *
  * Usage: selkv_c_demo IN OUT
  *   IN:  int32 B, H, G, d, n, W; then float32 K [B,H,n,d], V [B,H,n,d],
@@ -129,6 +132,10 @@ int main(int argc, char** argv) {
   SELKV_OK_(selkv_bias(&p, attn, kept, evicted, target, gate, bias, ws, ws_bytes, st));
   SELKV_OK_(selkv_decode_attn(&p, q, K_out, V_out, bias, (int32_t)m, out, ws, ws_bytes, st));
 
+  /* the allocation-free decode (the library's own scratch) must match the workspace call bit for bit */
+  float* out2 = (float*)dev_alloc(qd_bytes);
+  SELKV_OK_(selkv_decode_attn_noalloc(&p, q, K_out, V_out, bias, (int32_t)m, out2, st));
+
   /* the fused call must reproduce selkv_merge + selkv_bias bit for bit */
   void* K_out2 = dev_alloc(B * H * m * d * sizeof(float));
   void* V_out2 = dev_alloc(B * H * m * d * sizeof(float));
@@ -143,7 +150,7 @@ int main(int argc, char** argv) {
   const struct { const void *a, *b; size_t bytes; const char* name; } same[] = {
       {K_out, K_out2, B * H * m * d * sizeof(float), "K_out"}, {V_out, V_out2, B * H * m * d * sizeof(float), "V_out"},
       {target, target2, B * H * ne * sizeof(int32_t), "target"}, {gate, gate2, B * H * ne * sizeof(float), "gate"},
-      {bias, bias2, B * H * m * sizeof(float), "bias"}};
+      {bias, bias2, B * H * m * sizeof(float), "bias"}, {out, out2, qd_bytes, "decode out (noalloc)"}};
   for (size_t i = 0; i < sizeof(same) / sizeof(same[0]); ++i) {
     char* ha = (char*)malloc(same[i].bytes > 0 ? same[i].bytes : 1);
     char* hb = (char*)malloc(same[i].bytes > 0 ? same[i].bytes : 1);
@@ -151,7 +158,7 @@ int main(int argc, char** argv) {
     HIP_OK(hipMemcpy(ha, same[i].a, same[i].bytes, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(hb, same[i].b, same[i].bytes, hipMemcpyDeviceToHost));
     if (memcmp(ha, hb, same[i].bytes) != 0) {
-      fprintf(stderr, "selkv_merge_bias differs from selkv_merge + selkv_bias in %s\n", same[i].name);
+      fprintf(stderr, "two calls that must agree bit for bit differ in %s\n", same[i].name);
       return 7;
     }
     free(ha);

@@ -1181,6 +1181,55 @@ def test_random_configs_stagewise(S, seed):
         assert torch.equal(v, sep[k]), k
 
 
+# ------------------------------------------------------------------ all-pairs routing with more than 65535 kept slots
+def test_full_cosine_three_sort_passes(S):
+    """70000 kept slots: the slot keys 0 .. m need 17 bits, so the grouping
+    by target slot takes three 8-bit radix passes.  Sampled rows are checked
+    against the float64 cosine argmax (near-ties within 1e-6 counted); then
+    every slot's merged value and bias against the oracle's Eq. 5 / Eq. 6
+    fed the GPU's own targets and gates, which holds only if every slot's
+    list is exactly its tokens."""
+    case = dict(batch=1, H=1, G=2, d=64, n=140000, W=16, dtype="bf16")
+    t = synth.random_case(140001, batch=1, n_heads_kv=1, group=2, head_dim=64, seq_len=case["n"], window=16,
+                          dtype="bf16", clusters=8, device=DEV)
+    K, V, Q = t["K"], t["V"], t["Qwin"]
+    p = make_params(S, case, budget_ratio=0.5)
+    comp = S.Compressor(p, DEV).run(K, V, Q)
+    pf = make_params(S, case, budget_ratio=0.5, route_mode="full_cosine")
+    ws = S.workspace(pf, S.CALL_MERGE, DEV)
+    K_out, V_out = torch.empty_like(comp.K_out), torch.empty_like(comp.V_out)
+    target, gate = torch.empty_like(comp.target), torch.empty_like(comp.gate)
+    S.merge(pf, K, V, comp.attn, comp.vnorm, comp.kept, comp.evicted, K_out, V_out, target, gate, ws)
+    bias = torch.empty_like(comp.bias)
+    S.bias(pf, comp.attn, comp.kept, comp.evicted, target, gate, bias, ws)
+    torch.cuda.synchronize()
+    m = comp.m
+    assert m > 65535
+    kept, ev = comp.kept[0, 0].cpu().numpy(), comp.evicted[0, 0].cpu().numpy()
+    tg, g = target[0, 0].cpu().numpy(), gate[0, 0].cpu().double().numpy()
+    assert ((tg >= 0) & (tg < m)).all()
+    V64, K64 = np64(V[0, 0]), np64(K[0, 0])
+    vk = V64[kept]
+    nk = np.linalg.norm(vk, axis=1)
+    rows = np.random.default_rng(3).choice(len(ev), 256, replace=False)
+    ties = 0
+    for r in rows:
+        vj = V64[ev[r]]
+        cos = (vk @ vj) / (nk * np.linalg.norm(vj))
+        best = int(np.argmax(cos))
+        if tg[r] != best:
+            assert cos[tg[r]] >= cos[best] - NEAR_TIE * abs(cos[best]), f"row {ev[r]}"
+            ties += 1
+    a = comp.attn[0, 0].cpu().double().numpy()
+    _, v_out, _ = O.merge(K64, V64, a, kept, ev, tg, g)
+    assert_close_rows(np64(V_out[0, 0]), v_out, TOL["bf16"], "V_out")
+    want = O.ratio_bias(a, kept, ev, tg, g, float(np.float32(p.alpha)))
+    # fp32 sums of the same fp32 inputs: any slot holding a wrong list would be off by far more
+    assert (np.abs(np64(bias[0, 0]) - want) <= 1e-5 * (1 + np.abs(want))).all()
+    assert torch.equal(K_out[0, 0].cpu(), K[0, 0].cpu()[torch.as_tensor(kept)])
+    record("full_cosine_three_sort_passes", "n 140000, m 70000", route_ties=ties)
+
+
 # ------------------------------------------------------------------ all-pairs routing at the full ctx100k size, sampled
 def test_full_cosine_full_size_sampled(S):
     """a9 at the bench's size: one ctx100k layer (8 KV heads, 76800 evicted x
