@@ -37,7 +37,7 @@ constexpr int kKeysPerStep = 4 * kUnroll;        // per wave
 #endif
 constexpr int kTargetBlocks = SELKV_DECODE_TARGET_BLOCKS;   // workgroups per launch (one per CU)
 constexpr int kMaxSplit = 1024;
-constexpr int kReduceThreads = 512;
+constexpr int kReduceThreads = 256;   // 256 measured 0.4 - 0.6 us faster per call than 512 or 128
 
 template <typename T, int D>
 __device__ __forceinline__ void load_slice(const char* row, int col, float (&x)[Slice<T, D>::kElems]) {
