@@ -491,6 +491,32 @@ def test_union_ratio_bias_single_head_is_per_head():
     assert np.allclose(one, O.ratio_bias(a, kept, ev, tg, g, 0.5), rtol=1e-14, atol=1e-15)
 
 
+def test_compress_union_reduces_to_per_head_cases():
+    """The union-mode driver against the cases the per-head pipeline fixes:
+    one KV head is exactly compress_head (a union of one set, R averaged over
+    one head); KV heads with identical keys, values and queries pick the same
+    set, route alike and share one R, so every head equals compress_head."""
+    r = rng(21)
+    n, d, G, W = 96, 8, 2, 8
+    k = r.standard_normal((1, n, d)) / 3
+    v = r.standard_normal((1, n, d))
+    q = r.standard_normal((G, W, d)) / 3
+    for route in ("bucket", "full_cosine"):
+        one = O.compress_union(k, v, q, group=G, window=W, bucket=8, budget_ratio=0.3, route_mode=route)
+        ref = O.compress_head(k[0], v[0], q, window=W, bucket=8, budget_ratio=0.3, route_mode=route)
+        for key in ("kept", "evicted", "target"):
+            np.testing.assert_array_equal(one[key][0], ref[key], err_msg=key)
+        for key in ("gate", "v_out", "bias", "score", "attn"):
+            np.testing.assert_allclose(one[key][0], ref[key], rtol=1e-13, atol=1e-15, err_msg=key)
+        three = O.compress_union(np.repeat(k, 3, 0), np.repeat(v, 3, 0), np.tile(q, (3, 1, 1)), group=G, window=W,
+                                 bucket=8, budget_ratio=0.3, route_mode=route)
+        for h in range(3):
+            np.testing.assert_array_equal(three["kept"][h], ref["kept"])
+            np.testing.assert_array_equal(three["target"][h], ref["target"])
+            np.testing.assert_allclose(three["bias"][h], ref["bias"], rtol=1e-13, atol=1e-15)
+            np.testing.assert_allclose(three["v_out"][h], ref["v_out"], rtol=1e-13, atol=1e-15)
+
+
 # ------------------------------------------------------------------ RoPE repositioning (Eq. 7)
 def test_rope_reposition_hand_worked():
     c = GOLD["rope_reposition"]

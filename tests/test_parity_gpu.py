@@ -611,6 +611,25 @@ def union_oracle_compare(S, p, comp, K64, V64, Q64, b, tol):
     return totals
 
 
+@pytest.mark.parametrize("case", UNION, ids=[f"union{i}" for i in range(len(UNION))])
+def test_gqa_union_end_to_end(S, case):
+    """The whole union-mode pipeline (fused merge + bias) on the GPU's own
+    scores against the oracle's union mode: the shared kept set but for
+    near-ties of the trim or of a head's own top-m_s, per-head targets,
+    gates and merged values, and the head-averaged bias."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 5 + case["H"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"], device=DEV)
+    p = make_params(S, case, select_mode="union", **kw)
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    K64, V64, Q64 = np64(t["K"]), np64(t["V"]), np64(t["Qwin"])
+    for b in range(case["batch"]):
+        counts = union_oracle_compare(S, p, comp, K64, V64, Q64, b, TOL[case["dtype"]])
+        record("gqa_union_end_to_end", f"{case} {kw} b{b}", **counts)
+
+
 def test_gqa_union_end_to_end_llama_layer(S):
     """The whole union-mode compression of a Llama-shaped layer on the GPU
     against the oracle's union mode (float64 scores, float64 trim mean):
@@ -1010,6 +1029,52 @@ def test_coattn_end_to_end_llama_layer(S):
         counts = compare_end_to_end(gpu, ch, K64[0, h], w.seq_len, Bk, TOL[w.dtype], float(np.float32(p_co.alpha)),
                                     route_key=lambda j, i, A=A: float(A[:, i] @ A[:, j]))
         record("coattn_end_to_end", f"llama_layer n=4096 h{h}", **counts)
+
+
+# ------------------------------------------------------------------ alternative modes end to end
+def _oracle_mode_compare(S, p, comp, case, K64, V64, Q64, tag):
+    """Every (sequence, KV head) of the GPU's whole pipeline in p's mode
+    against compress_head in the same mode (keys merged with the Eq. 5
+    weights when p.merge_keys is set), near-ties counted."""
+    route = {S.ROUTE_BUCKET: "bucket", S.ROUTE_FULL_COSINE: "full_cosine", S.ROUTE_BUCKET_NEAREST: "bucket_nearest",
+             S.ROUTE_COATTN: "coattn"}[p.route_mode]
+    G, Bk = case["G"], p.bucket
+    tol, alpha = TOL[case["dtype"]], float(np.float32(p.alpha))
+    for b in range(case["batch"]):
+        for h in range(case["H"]):
+            ch = O.compress_head(K64[b, h], V64[b, h], Q64[b, h * G:(h + 1) * G], window=case["W"],
+                                 budget_ratio=p.budget_ratio, bucket=Bk, gate_mode=GATE[p.gate_mode],
+                                 gate_threshold=float(np.float32(p.gate_threshold)),
+                                 gate_temperature=float(np.float32(p.gate_temperature)), route_mode=route)
+            if p.merge_keys:
+                ch["k_out"], _, _ = O.merge(K64[b, h], V64[b, h], ch["attn"], ch["kept"], ch["evicted"],
+                                            ch["target"], ch["gate"], merge_keys=True)
+            key = None
+            if route == "coattn":
+                A = O.window_attention_group(Q64[b, h * G:(h + 1) * G], K64[b, h], oracle_scale(p))
+                key = lambda j, i, A=A: float(A[:, i] @ A[:, j])
+            counts = compare_end_to_end(gpu_head(comp, b, h), ch, K64[b, h], case["n"], Bk, tol, alpha, route_key=key,
+                                        local=route in ("bucket", "coattn"), keys_merged=bool(p.merge_keys))
+            record(tag, f"{case} b{b} h{h}", **counts)
+
+
+@pytest.mark.parametrize("case", READINGS + [dict(c, route_mode="coattn") for c in COATTN],
+                         ids=[f"reading{i}" for i in range(len(READINGS))] + [f"coattn{i}" for i in range(len(COATTN))])
+def test_alternative_modes_end_to_end(S, case):
+    """The nearest-kept fallback, merged keys and co-attention routing run
+    as whole GPU pipelines (score, select, [route,] fused merge + bias) on
+    the GPU's own intermediate results, against the oracle's pipeline in the
+    same mode."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 17 + 9, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=6, device=DEV)
+    p = make_params(S, case, **kw)
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    _oracle_mode_compare(S, p, comp, dict(case, **kw), np64(t["K"]), np64(t["V"]), np64(t["Qwin"]),
+                         "alternative_modes_end_to_end")
 
 
 # ------------------------------------------------------------------ fused merge + bias (steps 3 - 6 in one pass)
