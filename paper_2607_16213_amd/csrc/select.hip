@@ -1,13 +1,18 @@
 // selkv_select: per-head top-m_s selection of Sec. 3.3 (Eq. 2).
 //
 // One workgroup (16 waves) per KV head.  Scores are mapped to order-
-// preserving 32-bit keys; an MSB-first radix select finds the m_s-th largest
-// key T and how many keys equal to T must be taken:
-//   pass 1   histogram of the top 12 bits (4096 LDS bins, integer atomics)
-//   pass 2   the keys of the bin holding T (a few percent of the head) are
-//            copied into LDS, and the low 20 bits are resolved there in two
-//            10-bit passes; a bin too large for LDS is resolved with two
-//            more global passes instead
+// preserving 32-bit keys; a radix select finds the m_s-th largest key T and
+// how many keys equal to T must be taken, on the offsets d = key - min key:
+//   pass 0   the head's smallest and largest key
+//   pass 1   histogram of d >> s over 4096 LDS bins (integer atomics), s the
+//            smallest shift that fits the head's key range into them, so
+//            the bins span the scores actually present
+//   pass 2   the keys of the bin holding T (a few hundred for the scores
+//            the workloads produce) are copied into LDS, and the s low bits
+//            are resolved there in passes of at most 10 bits; a bin too
+//            large for LDS is resolved with global passes instead
+// Scores that concentrate in a narrow range (the usual case) would otherwise
+// put nearly every key of a head into one top-bits bin, one LDS counter.
 // A single ordered pass then keeps every key > T and the first `need` keys
 // == T (lowest positions win ties), compacting kept and evicted positions in
 // ascending order with one block prefix sum per 4096-key chunk.  The m_r'
@@ -27,9 +32,11 @@ static_assert(kChunk < 65536, "packed scan fields are 16 bits");
 constexpr int kHistBatch = 16;    // score loads in flight per thread
 constexpr int kTopBits = 12;
 constexpr int kTopBins = 1 << kTopBits;
-constexpr int kLowBits = 10;      // the two passes over the low 20 bits
+constexpr int kLowBits = 10;      // bits per pass below the top bins
 constexpr int kCandCap = 12288;   // keys of T's top bin held in LDS (48 KB)
-static_assert(kTopBits + 2 * kLowBits == 32, "the passes cover the 32-bit key");
+// a key range of up to 2^32 - 1 fits the top bins at a shift of at most 20,
+// which two low passes resolve
+static_assert(kTopBits + 2 * kLowBits == 32, "two low passes cover the bits below the top bins");
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -92,19 +99,20 @@ __device__ Pick find_bin(const int* hist, int nbins, int need, int* scan_lds, Pi
   return r;
 }
 
-// Histogram of digit (key >> shift) & (nbins - 1) over the keys matching
-// prefix under mask: from the global scores (LDS_SRC false) or the staged keys.
+// Histogram of digit (d >> shift) & (nbins - 1), d = key - base, over the
+// keys whose d matches prefix under mask: from the global scores (LDS_SRC
+// false) or the staged offsets (which are d already).
 template <bool LDS_SRC>
-__device__ void histogram(const float* s, const uint32_t* cand, int count, int shift, int nbins, uint32_t mask,
-                          uint32_t prefix, int* hist) {
+__device__ void histogram(const float* s, const uint32_t* cand, int count, uint32_t base, int shift, int nbins,
+                          uint32_t mask, uint32_t prefix, int* hist) {
   const int tid = threadIdx.x;
   for (int b = tid; b < nbins; b += kThreads) hist[b] = 0;
   __syncthreads();
   const uint32_t dmask = (uint32_t)nbins - 1u;
   if constexpr (LDS_SRC) {
     for (int j = tid; j < count; j += kThreads) {
-      const uint32_t key = cand[j];
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1);
+      const uint32_t d = cand[j];
+      if ((d & mask) == prefix) atomicAdd(&hist[(d >> shift) & dmask], 1);
     }
   } else {
     for (int j0 = tid; j0 < count; j0 += kThreads * kHistBatch) {
@@ -113,11 +121,46 @@ __device__ void histogram(const float* s, const uint32_t* cand, int count, int s
       for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
 #pragma unroll
       for (int u = 0; u < kHistBatch; ++u) {
-        const uint32_t key = order_key(v[u]);
-        if (j0 + u * kThreads < count && (key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1);
+        const uint32_t d = order_key(v[u]) - base;
+        if (j0 + u * kThreads < count && (d & mask) == prefix) atomicAdd(&hist[(d >> shift) & dmask], 1);
       }
     }
   }
+  __syncthreads();
+}
+
+// Smallest and largest key of the head, visible to every thread.
+__device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& kmin, uint32_t& kmax) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint32_t lo = 0xffffffffu, hi = 0u;
+  for (int j0 = tid; j0 < count; j0 += kThreads * kHistBatch) {
+    float v[kHistBatch];
+#pragma unroll
+    for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
+#pragma unroll
+    for (int u = 0; u < kHistBatch; ++u) {
+      const uint32_t key = order_key(v[u]);   // past the end: the last key again
+      lo = min(lo, key);
+      hi = max(hi, key);
+    }
+  }
+  for (int o = 32; o >= 1; o >>= 1) {
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, o, 64));
+    hi = max(hi, (uint32_t)__shfl_xor((int)hi, o, 64));
+  }
+  if (lane == 0) {
+    red[wave] = lo;
+    red[kWaves + wave] = hi;
+  }
+  __syncthreads();
+  lo = red[0];
+  hi = red[kWaves];
+  for (int w = 1; w < kWaves; ++w) {
+    lo = min(lo, red[w]);
+    hi = max(hi, red[kWaves + w]);
+  }
+  kmin = lo;
+  kmax = hi;
   __syncthreads();
 }
 
@@ -135,18 +178,23 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
   __shared__ Pick sh_pick;
   __shared__ int sh_pos;
 
-  // ---- radix select of the ms-th largest key
-  uint32_t prefix = 0u, mask = 0u;
+  // ---- radix select of the ms-th largest key, on d = key - kmin
+  __shared__ uint32_t red[2 * kWaves];
+  uint32_t kmin = 0u, prefix = 0u, mask = 0u;
   int need = ms;
   if (ms > 0) {
-    histogram<false>(s, nullptr, n_cand, 32 - kTopBits, kTopBins, 0u, 0u, hist);
+    uint32_t kmax;
+    key_range(s, n_cand, red, kmin, kmax);
+    int hi_bit = 0;   // the smallest shift that fits d into the top bins
+    while (hi_bit < 32 && ((kmax - kmin) >> hi_bit) >= (uint32_t)kTopBins) ++hi_bit;
+    histogram<false>(s, nullptr, n_cand, kmin, hi_bit, kTopBins, 0u, 0u, hist);
     Pick pk = find_bin(hist, kTopBins, need, scan_lds, &sh_pick);
-    prefix = pk.bin << (32 - kTopBits);
-    mask = ~0u << (32 - kTopBits);
+    prefix = pk.bin << hi_bit;
+    mask = ~0u << hi_bit;
     need = pk.need;
     const bool staged = pk.count <= kCandCap;
-    if (staged) {
-      // copy the bin's keys into LDS (order is irrelevant to the threshold)
+    if (staged && hi_bit > 0) {
+      // copy the bin's offsets into LDS (order is irrelevant to the threshold)
       if (tid == 0) sh_pos = 0;
       __syncthreads();
       for (int j0 = tid; j0 < n_cand; j0 += kThreads * kHistBatch) {
@@ -155,28 +203,33 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
         for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, n_cand - 1)];
 #pragma unroll
         for (int u = 0; u < kHistBatch; ++u) {
-          const uint32_t key = order_key(v[u]);
-          const bool hit = j0 + u * kThreads < n_cand && (key & mask) == prefix;
+          const uint32_t d = order_key(v[u]) - kmin;
+          const bool hit = j0 + u * kThreads < n_cand && (d & mask) == prefix;
           const uint64_t bal = __ballot(hit);
           if (bal) {                              // wave-uniform
             int base = 0;
             if (lane == 0) base = atomicAdd(&sh_pos, __popcll(bal));
             base = __shfl(base, 0, 64);
             const int at = base + __popcll(bal & ((1ull << lane) - 1ull));
-            if (hit && at < kCandCap) cand[at] = key;
+            if (hit && at < kCandCap) cand[at] = d;
           }
         }
       }
       __syncthreads();
     }
-    for (int shift = 32 - kTopBits - kLowBits; shift >= 0; shift -= kLowBits) {
-      if (staged) histogram<true>(nullptr, cand, pk.count, shift, 1 << kLowBits, mask, prefix, hist);
-      else histogram<false>(s, nullptr, n_cand, shift, 1 << kLowBits, mask, prefix, hist);
-      const Pick q = find_bin(hist, 1 << kLowBits, need, scan_lds, &sh_pick);
+    // the hi_bit low bits of d, at most kLowBits per pass
+    while (hi_bit > 0) {
+      const int shift = hi_bit > kLowBits ? hi_bit - kLowBits : 0;
+      const int nbins = 1 << (hi_bit - shift);
+      if (staged) histogram<true>(nullptr, cand, pk.count, 0u, shift, nbins, mask, prefix, hist);
+      else histogram<false>(s, nullptr, n_cand, kmin, shift, nbins, mask, prefix, hist);
+      const Pick q = find_bin(hist, nbins, need, scan_lds, &sh_pick);
       prefix |= q.bin << shift;
-      mask |= ((1u << kLowBits) - 1u) << shift;
+      mask |= ((uint32_t)nbins - 1u) << shift;
       need = q.need;
+      hi_bit = shift;
     }
+    prefix += kmin;   // the threshold key
   } else {
     prefix = 0xffffffffu;  // nothing is strictly greater; take no ties
     need = 0;

@@ -1157,36 +1157,50 @@ def test_merge_bias_fused_equals_merge_then_bias(S, case):
             record("fused_vs_oracle", f"{case} {kw} b{b} h{h}", **counts)
 
 
-# ------------------------------------------------------------------ selection: the threshold's top-12-bit bin
+# ------------------------------------------------------------------ selection: the threshold's bin
 def _select_case(rng, kind):
-    """(n, m, scores [2, n - 16] fp32) for a selection whose threshold falls in
-    a top-12-bit bin of a chosen population (values in [1, 1.1) share sign,
-    exponent and the top three mantissa bits)."""
+    """(n, m, scores [2, n - 16] fp32) for a selection whose threshold falls
+    in a bin of a chosen population.  The kernel bins the offsets of the
+    order-preserving keys from the head's smallest key into 4096 bins whose
+    width fits the head's key range, stages the threshold's bin in LDS when it
+    holds at most 12288 keys, and resolves the remaining low bits there (or in
+    global passes) at most 10 bits at a time."""
     if kind in ("at_cap", "over_cap"):
+        # a cluster within 8 ulps of 1.0 (one bin: the range reaches 100) holding the threshold
         inbin = 12288 if kind == "at_cap" else 12289
-        hi = 7712
-        n_cand = inbin + hi
-        s = np.concatenate([1.0 + 0.1 * rng.random((2, inbin)), 4.0 + rng.random((2, hi))], axis=1)
+        hi, top = 7712, 10
+        n_cand = inbin + hi + top
+        clus = np.float32(1.0) + np.float32(2.0 ** -23) * rng.integers(0, 8, (2, inbin)).astype(np.float32)
+        s = np.concatenate([clus, 4.0 + rng.random((2, hi)), np.full((2, top), 100.0)], axis=1)
         s = np.stack([rng.permutation(r) for r in s])
-        ms = hi + 5000
-    elif kind == "all_equal":
+        ms = top + hi + 5000
+    elif kind == "all_equal":       # zero key range: no low pass, ties decide
         n_cand, ms = 30000, 7000
         s = np.full((2, n_cand), 0.75)
-    else:   # five distinct values in one (staged) bin, many exact ties at the threshold
+    elif kind == "ties":            # five values 8 ulps apart: exact bins, many ties at the threshold
         n_cand, ms = 10000, 4000
         vals = np.float32(1.0) + np.float32(2.0 ** -20) * np.arange(5, dtype=np.float32)
         s = vals[rng.integers(0, 5, (2, n_cand))]
+    elif kind == "one_low_pass":    # 20000 consecutive floats: bins of 8 keys, one 3-bit low pass
+        n_cand, ms = 20000, 6000
+        s = np.float32(1.0) + np.float32(2.0 ** -23) * np.stack([rng.permutation(n_cand) for _ in range(2)]).astype(np.float32)
+    else:                           # "mixed_sign": keys span nearly 2^32, two full low passes
+        n_cand, ms = 30000, 9000
+        s = np.stack([np.concatenate([-np.exp(rng.normal(0, 20, n_cand // 2)), np.exp(rng.normal(0, 20, n_cand // 2))])
+                      for _ in range(2)])
+        s = np.stack([rng.permutation(r) for r in s.astype(np.float32)])
     n = n_cand + 16
-    return n, ms + 16, s.astype(np.float32)
+    return n, ms + 16, np.asarray(s, dtype=np.float32)
 
 
-@pytest.mark.parametrize("kind", ["at_cap", "over_cap", "all_equal", "ties"])
+@pytest.mark.parametrize("kind", ["at_cap", "over_cap", "all_equal", "ties", "one_low_pass", "mixed_sign"])
 def test_select_threshold_bin_staged_or_not(S, kind):
-    """The m_s-th largest score is found from a 12-bit histogram, then in LDS
-    when its bin holds at most 12288 keys and with two more passes over the
-    scores otherwise; either way the kept and evicted lists are the oracle's
-    bit for bit (equal scores: the lower position wins)."""
-    rng = np.random.default_rng({"at_cap": 1, "over_cap": 2, "all_equal": 3, "ties": 4}[kind])
+    """Whichever way the threshold's bin is resolved (staged in LDS or by
+    passes over the scores, with zero, one or two low passes), the kept and
+    evicted lists are the oracle's bit for bit (equal scores: the lower
+    position wins)."""
+    rng = np.random.default_rng({"at_cap": 1, "over_cap": 2, "all_equal": 3, "ties": 4, "one_low_pass": 5,
+                                 "mixed_sign": 6}[kind])
     n, m, s = _select_case(rng, kind)
     p = S.params(batch=1, n_heads_kv=2, group=1, head_dim=64, seq_len=n, window=8, kv_dtype="fp32",
                  budget_ratio=(m + 0.5) / n)
