@@ -3,7 +3,10 @@
 // One workgroup (16 waves) per KV head.  Scores are mapped to order-
 // preserving 32-bit keys; a radix select finds the m_s-th largest key T and
 // how many keys equal to T must be taken, on the offsets d = key - min key:
-//   pass 0   the head's smallest and largest key
+//   pass 0   the head's smallest and largest key above that of -inf, and
+//            how many keys lie above it (-inf marks candidates that must not
+//            be chosen; when fewer than m_s keys lie above, every key and
+//            the whole key range are used instead)
 //   pass 1   histogram of d >> s over 4096 LDS bins (integer atomics), s the
 //            smallest shift that fits the head's key range into them, so
 //            the bins span the scores actually present
@@ -37,6 +40,8 @@ constexpr int kCandCap = 12288;   // keys of T's top bin held in LDS (48 KB)
 // a key range of up to 2^32 - 1 fits the top bins at a shift of at most 20,
 // which two low passes resolve
 static_assert(kTopBits + 2 * kLowBits == 32, "two low passes cover the bits below the top bins");
+
+constexpr uint32_t kNegInfKey = 0x007fffffu;   // order_key(-inf)
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -100,11 +105,11 @@ __device__ Pick find_bin(const int* hist, int nbins, int need, int* scan_lds, Pi
 }
 
 // Histogram of digit (d >> shift) & (nbins - 1), d = key - base, over the
-// keys whose d matches prefix under mask: from the global scores (LDS_SRC
-// false) or the staged offsets (which are d already).
+// keys >= kfloor whose d matches prefix under mask: from the global scores
+// (LDS_SRC false) or the staged offsets (which are d already, all admitted).
 template <bool LDS_SRC>
-__device__ void histogram(const float* s, const uint32_t* cand, int count, uint32_t base, int shift, int nbins,
-                          uint32_t mask, uint32_t prefix, int* hist) {
+__device__ void histogram(const float* s, const uint32_t* cand, int count, uint32_t kfloor, uint32_t base, int shift,
+                          int nbins, uint32_t mask, uint32_t prefix, int* hist) {
   const int tid = threadIdx.x;
   for (int b = tid; b < nbins; b += kThreads) hist[b] = 0;
   __syncthreads();
@@ -121,46 +126,57 @@ __device__ void histogram(const float* s, const uint32_t* cand, int count, uint3
       for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
 #pragma unroll
       for (int u = 0; u < kHistBatch; ++u) {
-        const uint32_t d = order_key(v[u]) - base;
-        if (j0 + u * kThreads < count && (d & mask) == prefix) atomicAdd(&hist[(d >> shift) & dmask], 1);
+        const uint32_t key = order_key(v[u]), d = key - base;
+        if (j0 + u * kThreads < count && key >= kfloor && (d & mask) == prefix)
+          atomicAdd(&hist[(d >> shift) & dmask], 1);
       }
     }
   }
   __syncthreads();
 }
 
-// Smallest and largest key of the head, visible to every thread.
-__device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& kmin, uint32_t& kmax) {
+// Smallest and largest key above the key of -inf, and how many keys are
+// above it, visible to every thread (lo > hi when there are none).
+__device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& kmin, uint32_t& kmax, int& above) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   uint32_t lo = 0xffffffffu, hi = 0u;
+  int c = 0;
   for (int j0 = tid; j0 < count; j0 += kThreads * kHistBatch) {
     float v[kHistBatch];
 #pragma unroll
     for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
 #pragma unroll
     for (int u = 0; u < kHistBatch; ++u) {
-      const uint32_t key = order_key(v[u]);   // past the end: the last key again
-      lo = min(lo, key);
-      hi = max(hi, key);
+      const uint32_t key = order_key(v[u]);
+      if (j0 + u * kThreads < count && key > kNegInfKey) {
+        lo = min(lo, key);
+        hi = max(hi, key);
+        ++c;
+      }
     }
   }
   for (int o = 32; o >= 1; o >>= 1) {
     lo = min(lo, (uint32_t)__shfl_xor((int)lo, o, 64));
     hi = max(hi, (uint32_t)__shfl_xor((int)hi, o, 64));
+    c += __shfl_xor(c, o, 64);
   }
   if (lane == 0) {
     red[wave] = lo;
     red[kWaves + wave] = hi;
+    red[2 * kWaves + wave] = (uint32_t)c;
   }
   __syncthreads();
   lo = red[0];
   hi = red[kWaves];
+  c = (int)red[2 * kWaves];
   for (int w = 1; w < kWaves; ++w) {
     lo = min(lo, red[w]);
     hi = max(hi, red[kWaves + w]);
+    c += (int)red[2 * kWaves + w];
   }
   kmin = lo;
   kmax = hi;
+  above = c;
   __syncthreads();
 }
 
@@ -179,15 +195,26 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
   __shared__ int sh_pos;
 
   // ---- radix select of the ms-th largest key, on d = key - kmin
-  __shared__ uint32_t red[2 * kWaves];
+  __shared__ uint32_t red[3 * kWaves];
   uint32_t kmin = 0u, prefix = 0u, mask = 0u;
   int need = ms;
   if (ms > 0) {
     uint32_t kmax;
-    key_range(s, n_cand, red, kmin, kmax);
+    int above;
+    key_range(s, n_cand, red, kmin, kmax, above);
+    // With at least ms keys above -inf the threshold is one of them: those
+    // keys alone are binned (-inf marks what must not be chosen, e.g. the
+    // non-members of the GQA union, and would stretch the range over the
+    // whole key space).  Otherwise every key and the whole range are used.
+    uint32_t kfloor = kNegInfKey + 1u;
+    if (above < ms) {
+      kfloor = 0u;
+      kmin = 0u;
+      kmax = 0xffffffffu;
+    }
     int hi_bit = 0;   // the smallest shift that fits d into the top bins
     while (hi_bit < 32 && ((kmax - kmin) >> hi_bit) >= (uint32_t)kTopBins) ++hi_bit;
-    histogram<false>(s, nullptr, n_cand, kmin, hi_bit, kTopBins, 0u, 0u, hist);
+    histogram<false>(s, nullptr, n_cand, kfloor, kmin, hi_bit, kTopBins, 0u, 0u, hist);
     Pick pk = find_bin(hist, kTopBins, need, scan_lds, &sh_pick);
     prefix = pk.bin << hi_bit;
     mask = ~0u << hi_bit;
@@ -203,8 +230,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
         for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, n_cand - 1)];
 #pragma unroll
         for (int u = 0; u < kHistBatch; ++u) {
-          const uint32_t d = order_key(v[u]) - kmin;
-          const bool hit = j0 + u * kThreads < n_cand && (d & mask) == prefix;
+          const uint32_t key = order_key(v[u]), d = key - kmin;
+          const bool hit = j0 + u * kThreads < n_cand && key >= kfloor && (d & mask) == prefix;
           const uint64_t bal = __ballot(hit);
           if (bal) {                              // wave-uniform
             int base = 0;
@@ -221,8 +248,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
     while (hi_bit > 0) {
       const int shift = hi_bit > kLowBits ? hi_bit - kLowBits : 0;
       const int nbins = 1 << (hi_bit - shift);
-      if (staged) histogram<true>(nullptr, cand, pk.count, 0u, shift, nbins, mask, prefix, hist);
-      else histogram<false>(s, nullptr, n_cand, kmin, shift, nbins, mask, prefix, hist);
+      if (staged) histogram<true>(nullptr, cand, pk.count, 0u, 0u, shift, nbins, mask, prefix, hist);
+      else histogram<false>(s, nullptr, n_cand, kfloor, kmin, shift, nbins, mask, prefix, hist);
       const Pick q = find_bin(hist, nbins, need, scan_lds, &sh_pick);
       prefix |= q.bin << shift;
       mask |= ((uint32_t)nbins - 1u) << shift;

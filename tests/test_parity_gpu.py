@@ -1184,6 +1184,15 @@ def _select_case(rng, kind):
     elif kind == "one_low_pass":    # 20000 consecutive floats: bins of 8 keys, one 3-bit low pass
         n_cand, ms = 20000, 6000
         s = np.float32(1.0) + np.float32(2.0 ** -23) * np.stack([rng.permutation(n_cand) for _ in range(2)]).astype(np.float32)
+    elif kind == "minus_inf":       # -inf marks candidates that must not be chosen (the GQA union's non-members)
+        n_cand, ms = 40000, 9000
+        s = np.float32(1.0) + np.float32(0.01) * rng.random((2, n_cand)).astype(np.float32)
+        s[rng.random((2, n_cand)) < 0.4] = -np.inf
+    elif kind == "few_finite":      # fewer finite keys than m_s: the threshold is -inf, ties by position
+        n_cand, ms = 20000, 7000
+        s = np.full((2, n_cand), -np.inf, dtype=np.float32)
+        for r in range(2):
+            s[r, rng.choice(n_cand, 3000, replace=False)] = 1.0 + rng.random(3000)
     else:                           # "mixed_sign": keys span nearly 2^32, two full low passes
         n_cand, ms = 30000, 9000
         s = np.stack([np.concatenate([-np.exp(rng.normal(0, 20, n_cand // 2)), np.exp(rng.normal(0, 20, n_cand // 2))])
@@ -1193,14 +1202,15 @@ def _select_case(rng, kind):
     return n, ms + 16, np.asarray(s, dtype=np.float32)
 
 
-@pytest.mark.parametrize("kind", ["at_cap", "over_cap", "all_equal", "ties", "one_low_pass", "mixed_sign"])
+@pytest.mark.parametrize("kind", ["at_cap", "over_cap", "all_equal", "ties", "one_low_pass", "mixed_sign", "minus_inf",
+                                  "few_finite"])
 def test_select_threshold_bin_staged_or_not(S, kind):
     """Whichever way the threshold's bin is resolved (staged in LDS or by
-    passes over the scores, with zero, one or two low passes), the kept and
-    evicted lists are the oracle's bit for bit (equal scores: the lower
-    position wins)."""
+    passes over the scores, with zero, one or two low passes, over the keys
+    above -inf or over all keys), the kept and evicted lists are the
+    oracle's bit for bit (equal scores: the lower position wins)."""
     rng = np.random.default_rng({"at_cap": 1, "over_cap": 2, "all_equal": 3, "ties": 4, "one_low_pass": 5,
-                                 "mixed_sign": 6}[kind])
+                                 "mixed_sign": 6, "minus_inf": 7, "few_finite": 8}[kind])
     n, m, s = _select_case(rng, kind)
     p = S.params(batch=1, n_heads_kv=2, group=1, head_dim=64, seq_len=n, window=8, kv_dtype="fp32",
                  budget_ratio=(m + 0.5) / n)
