@@ -14,7 +14,8 @@ def pytest_configure(config):
 def pytest_terminal_summary(terminalreporter, exitstatus, config):
     """Near-tie accounting of the GPU parity tests: every comparison that
     allowed a near-tie records its counts, shown here even under -q and
-    written to gpurun_out/parity_record.json."""
+    written as parity_record.json to the run's output folder
+    (SELKV_RECORD_DIR, by default the one GPU runs hand back)."""
     try:
         from tests.parity_util import RECORDS
     except ImportError:
@@ -36,7 +37,7 @@ def pytest_terminal_summary(terminalreporter, exitstatus, config):
         worst_err = max(worst_err, float(r.get("score_rel_err", 0.0)))
     tr.write_line("totals: " + " ".join(f"{k}={v}" for k, v in totals.items())
                   + f" max score_rel_err={worst_err:.2e} over {len(RECORDS)} comparisons")
-    out = os.path.join(ROOT, "gpurun_out")
+    out = os.environ.get("SELKV_RECORD_DIR", os.path.join(ROOT, "gpurun_out"))
     try:
         os.makedirs(out, exist_ok=True)
         with open(os.path.join(out, "parity_record.json"), "w") as f:

@@ -13,7 +13,7 @@ GATE_ATOL = 1e-5                        # gates: fp32 arithmetic on exact inputs
 NEAR_TIE = 1e-6                         # relative score gap within which two choices count as tied
 
 # Near-tie counts of the parity tests, printed in pytest's terminal summary
-# (conftest.py) and written to gpurun_out/parity_record.json.
+# and written to parity_record.json (conftest.py).
 RECORDS = []
 
 
