@@ -1245,6 +1245,26 @@ def _random_config(seed):
     return case, kw
 
 
+def _random_mid_config(seed):
+    """Mid-size draws: several score chunks, select chunks and match tiles per
+    head, window rows up to 512, budgets up to 60%."""
+    rng = np.random.default_rng(77000 + seed)
+    d = int(rng.choice([64, 128]))
+    n = int(rng.integers(1000, 24000))
+    W = int(rng.integers(1, 129))
+    G = int(rng.choice([1, 2, 4, 8]))
+    while G * W > 512:
+        W //= 2
+    case = dict(batch=int(rng.integers(1, 3)), H=int(rng.integers(1, 3)), G=G, d=d, n=n, W=W,
+                dtype=str(rng.choice(["fp32", "bf16"])))
+    kw = dict(bucket=int(rng.choice([8, 16, 32, 48, 64])), pool_kernel=int(rng.choice([1, 5, 9])),
+              recent=int(rng.integers(0, 65)), budget_ratio=float(rng.uniform(0.05, 0.6)),
+              gate_mode=int(rng.integers(0, 3)), gate_threshold=float(rng.choice([0.0, 0.2])),
+              gate_temperature=float(rng.choice([0.5, 1.0])), alpha=float(rng.uniform(0.1, 1.0)),
+              scale=float(rng.choice([0.0, 0.05])))
+    return case, kw
+
+
 @pytest.mark.parametrize("seed", range(64))
 def test_random_configs_stagewise(S, seed):
     """Randomly drawn shapes and parameters (batch, heads, group, d, n, W,
@@ -1253,7 +1273,16 @@ def test_random_configs_stagewise(S, seed):
     oracle's inputs matches it (indices bit-exact), one decode step over the
     oracle's cache matches, and the fused merge + bias call reproduces the
     separate calls bit for bit on the GPU's own chain."""
-    case, kw = _random_config(seed)
+    _random_check(S, seed, *_random_config(seed))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_mid_size_configs_stagewise(S, seed):
+    """As test_random_configs_stagewise, at 1000 - 24000 tokens per head."""
+    _random_check(S, seed, *_random_mid_config(seed))
+
+
+def _random_check(S, seed, case, kw):
     print(f"random config {seed}: {case} {kw}", flush=True)
     t = synth.random_case(seed * 31 + 7, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
                           head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
