@@ -1,24 +1,37 @@
 // selkv_select: per-head top-m_s selection of Sec. 3.3 (Eq. 2).
 //
 // One workgroup (16 waves) per KV head.  Scores are mapped to order-
-// preserving 32-bit keys; a radix select finds the m_s-th largest key T and
-// how many keys equal to T must be taken, on the offsets d = key - min key:
+// preserving 32-bit keys; the kernel finds the m_s-th largest key T and how
+// many keys equal to T must be taken (`need`), then compacts.
+//
+// Threshold, usual path (two reads of the scores in all):
+//   sample   4096 keys at evenly spaced positions; a histogram of the sample
+//            over its own key range gives a band of keys around the sample
+//            rank where T is expected (128 sample ranks on either side)
+//   band     one pass over the scores: keys above the band are counted per
+//            wave, keys inside it are staged in LDS with their positions
+//   resolve  when T lies inside the band and the band fits in LDS (nearly
+//            always), T and `need` are resolved among the staged keys by LDS
+//            radix passes, and the staged keys complete the per-wave counts
+// Heads of at most 12288 candidates stage every key and skip the sample.
+// Otherwise (a band that misses T or overflows, e.g. very many equal keys):
 //   pass 0   the head's smallest and largest key above that of -inf, and
 //            how many keys lie above it (-inf marks candidates that must not
 //            be chosen; when fewer than m_s keys lie above, every key and
 //            the whole key range are used instead)
-//   pass 1   histogram of d >> s over 4096 LDS bins (integer atomics), s the
-//            smallest shift that fits the head's key range into them, so
-//            the bins span the scores actually present
-//   pass 2   the keys of the bin holding T (a few hundred for the scores
-//            the workloads produce) are copied into LDS, and the s low bits
-//            are resolved there in passes of at most 10 bits; a bin too
+//   pass 1   histogram of d >> s over 4096 LDS bins (integer atomics), d the
+//            offset from the smallest key and s the smallest shift that fits
+//            the key range into them, so the bins span the scores present
+//   pass 2   the keys of the bin holding T are copied into LDS and the s low
+//            bits are resolved there in passes of at most 10 bits; a bin too
 //            large for LDS is resolved with global passes instead
-// Scores that concentrate in a narrow range (the usual case) would otherwise
-// put nearly every key of a head into one top-bits bin, one LDS counter.
-// A single ordered pass then keeps every key > T and the first `need` keys
-// == T (lowest positions win ties), compacting kept and evicted positions in
-// ascending order with one block prefix sum per 4096-key chunk.  The m_r'
+//   count    each wave counts its segment's keys > T and == T
+// Either way the result is the exact m_s-th largest key: the paths differ
+// only in cost.  Compaction: wave w owns one contiguous segment of the
+// candidates; the per-wave counts are prefixed once, and each wave walks its
+// segment keeping every key > T and the first `need` keys == T (lowest
+// positions win ties), ranking its keys with ballots, so kept and evicted
+// positions come out ascending with no barrier inside the walk.  The m_r'
 // recent positions are appended to the kept list.  Outputs do not depend on
 // scheduling: bitwise deterministic.
 #include "common.hpp"
@@ -29,9 +42,10 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
-constexpr int kPerThread = 4;                   // consecutive keys per thread in the compaction
-constexpr int kChunk = kThreads * kPerThread;
-static_assert(kChunk < 65536, "packed scan fields are 16 bits");
+constexpr int kIter = 256;        // keys of one wave step (four per lane: positions e * 64 + lane)
+constexpr int kRing = 8;          // wave steps whose loads are in flight together
+constexpr int kSample = 4096;     // sampled keys (four per thread)
+constexpr int kBandRanks = 128;   // sample ranks on either side of T's expected rank
 constexpr int kHistBatch = 16;    // score loads in flight per thread
 constexpr int kTopBits = 12;
 constexpr int kTopBins = 1 << kTopBits;
@@ -135,26 +149,11 @@ __device__ void histogram(const float* s, const uint32_t* cand, int count, uint3
   __syncthreads();
 }
 
-// Smallest and largest key above the key of -inf, and how many keys are
-// above it, visible to every thread (lo > hi when there are none).
-__device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& kmin, uint32_t& kmax, int& above) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint32_t lo = 0xffffffffu, hi = 0u;
-  int c = 0;
-  for (int j0 = tid; j0 < count; j0 += kThreads * kHistBatch) {
-    float v[kHistBatch];
-#pragma unroll
-    for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
-#pragma unroll
-    for (int u = 0; u < kHistBatch; ++u) {
-      const uint32_t key = order_key(v[u]);
-      if (j0 + u * kThreads < count && key > kNegInfKey) {
-        lo = min(lo, key);
-        hi = max(hi, key);
-        ++c;
-      }
-    }
-  }
+// Block-wide min / max / sum of the per-thread partial ranges, visible to
+// every thread.
+__device__ void reduce_range(uint32_t lo, uint32_t hi, int c, uint32_t* red, uint32_t& kmin, uint32_t& kmax,
+                             int& count) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int o = 32; o >= 1; o >>= 1) {
     lo = min(lo, (uint32_t)__shfl_xor((int)lo, o, 64));
     hi = max(hi, (uint32_t)__shfl_xor((int)hi, o, 64));
@@ -176,8 +175,94 @@ __device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& km
   }
   kmin = lo;
   kmax = hi;
-  above = c;
+  count = c;
   __syncthreads();
+}
+
+// Smallest and largest key above the key of -inf, and how many keys are
+// above it, visible to every thread (lo > hi when there are none).
+__device__ void key_range(const float* s, int count, uint32_t* red, uint32_t& kmin, uint32_t& kmax, int& above) {
+  const int tid = threadIdx.x;
+  uint32_t lo = 0xffffffffu, hi = 0u;
+  int c = 0;
+  for (int j0 = tid; j0 < count; j0 += kThreads * kHistBatch) {
+    float v[kHistBatch];
+#pragma unroll
+    for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, count - 1)];
+#pragma unroll
+    for (int u = 0; u < kHistBatch; ++u) {
+      const uint32_t key = order_key(v[u]);
+      if (j0 + u * kThreads < count && key > kNegInfKey) {
+        lo = min(lo, key);
+        hi = max(hi, key);
+        ++c;
+      }
+    }
+  }
+  reduce_range(lo, hi, c, red, kmin, kmax, above);
+}
+
+// The smallest shift that fits the key range [kmin, kmax] into the top bins.
+__device__ __forceinline__ int top_shift(uint32_t kmin, uint32_t kmax) {
+  int hb = 0;
+  while (hb < 32 && ((kmax - kmin) >> hb) >= (uint32_t)kTopBins) ++hb;
+  return hb;
+}
+
+// Walks the wave's segment [begin, end) of the scores: step t holds
+// positions begin + t * kIter + e * 64 + lane (e = 0 .. 3), so every load
+// instruction reads 256 contiguous bytes and the keys of a step ascend in
+// (e, lane) order.  The loads of kRing steps are issued together, the next
+// group's before the current group is handled.  f(t, v) gets the lane's four
+// scores of step t; reads past the end are clamped (the caller masks them by
+// position).
+template <class F>
+__device__ __forceinline__ void walk_segment(const float* s, int begin, int end, F&& f) {
+  const int lane = threadIdx.x & 63;
+  const int steps = (end - begin + kIter - 1) / kIter;
+  if (steps <= 0) return;
+  float cur[kRing][4], nxt[kRing][4];
+  auto load = [&](float (&v)[kRing][4], int g) {
+#pragma unroll
+    for (int r = 0; r < kRing; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[r][e] = s[min(begin + (g + r) * kIter + e * 64 + lane, end - 1)];
+  };
+  load(cur, 0);
+  for (int g = 0; g < steps; g += kRing) {
+    if (g + kRing < steps) load(nxt, g + kRing);
+#pragma unroll
+    for (int r = 0; r < kRing; ++r)
+      if (g + r < steps) f(g + r, cur[r]);
+#pragma unroll
+    for (int r = 0; r < kRing; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cur[r][e] = nxt[r][e];
+  }
+}
+
+// Resolves the need-th largest of the staged offsets cand[0 .. count) whose
+// values lie in [0, 2^32): the offset itself, and `need` becomes its rank
+// among the offsets equal to it.
+__device__ uint32_t resolve_staged(const uint32_t* cand, int count, uint32_t dmax, int& need, int* hist, int* scan_lds,
+                                   Pick* sh) {
+  int hb = top_shift(0u, dmax);
+  histogram<true>(nullptr, cand, count, 0u, 0u, hb, kTopBins, 0u, 0u, hist);
+  const Pick pk = find_bin(hist, kTopBins, need, scan_lds, sh);
+  uint32_t prefix = pk.bin << hb;
+  uint32_t mask = hb >= 32 ? 0u : ~0u << hb;
+  need = pk.need;
+  while (hb > 0) {
+    const int shift = hb > kLowBits ? hb - kLowBits : 0;
+    const int nbins = 1 << (hb - shift);
+    histogram<true>(nullptr, cand, count, 0u, 0u, shift, nbins, mask, prefix, hist);
+    const Pick q = find_bin(hist, nbins, need, scan_lds, sh);
+    prefix |= q.bin << shift;
+    mask |= ((uint32_t)nbins - 1u) << shift;
+    need = q.need;
+    hb = shift;
+  }
+  return prefix;
 }
 
 __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, int32_t* kept, int32_t* evicted,
@@ -186,129 +271,215 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
   const float* s = score + (size_t)head * n_cand;
   int32_t* kh = kept + (size_t)head * m;
   int32_t* eh = evicted + (size_t)head * (n - m);
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t below = (1ull << lane) - 1ull;
 
   __shared__ int hist[kTopBins];
-  __shared__ uint32_t cand[kCandCap];
+  __shared__ uint32_t cand[kCandCap];   // staged key offsets (the sample first)
+  __shared__ int cpos[kCandCap];        // their positions (band path)
   __shared__ int scan_lds[2 * kWaves + 1];
+  __shared__ uint32_t red[3 * kWaves];
+  __shared__ int wgt[kWaves], weq[kWaves];   // per wave: keys > T, keys == T in its segment
   __shared__ Pick sh_pick;
   __shared__ int sh_pos;
 
-  // ---- radix select of the ms-th largest key, on d = key - kmin
-  __shared__ uint32_t red[3 * kWaves];
-  uint32_t kmin = 0u, prefix = 0u, mask = 0u;
-  int need = ms;
+  // wave w owns candidates [w * seg, (w + 1) * seg)
+  const int seg = (n_cand + kWaves * kIter - 1) / (kWaves * kIter) * kIter;
+  const int wb = min(wave * seg, n_cand), we = min(wb + seg, n_cand);
+  if (tid < kWaves) {
+    wgt[tid] = 0;
+    weq[tid] = 0;
+  }
+
+  uint32_t T = 0xffffffffu;   // ms == 0: nothing is strictly greater, and no ties are taken
+  int need = 0;
   if (ms > 0) {
-    uint32_t kmax;
-    int above;
-    key_range(s, n_cand, red, kmin, kmax, above);
-    // With at least ms keys above -inf the threshold is one of them: those
-    // keys alone are binned (-inf marks what must not be chosen, e.g. the
-    // non-members of the GQA union, and would stretch the range over the
-    // whole key space).  Otherwise every key and the whole range are used.
-    uint32_t kfloor = kNegInfKey + 1u;
-    if (above < ms) {
-      kfloor = 0u;
-      kmin = 0u;
-      kmax = 0xffffffffu;
-    }
-    int hi_bit = 0;   // the smallest shift that fits d into the top bins
-    while (hi_bit < 32 && ((kmax - kmin) >> hi_bit) >= (uint32_t)kTopBins) ++hi_bit;
-    histogram<false>(s, nullptr, n_cand, kfloor, kmin, hi_bit, kTopBins, 0u, 0u, hist);
-    Pick pk = find_bin(hist, kTopBins, need, scan_lds, &sh_pick);
-    prefix = pk.bin << hi_bit;
-    mask = ~0u << hi_bit;
-    need = pk.need;
-    const bool staged = pk.count <= kCandCap;
-    if (staged && hi_bit > 0) {
-      // copy the bin's offsets into LDS (order is irrelevant to the threshold)
-      if (tid == 0) sh_pos = 0;
+    // ---- the band [lo, hi) of keys around T's expected place (hi = 2^32: no key above)
+    uint32_t lo = 0u;
+    uint64_t hi = 1ull << 32;
+    if (n_cand > kCandCap) {
+      uint32_t smin = 0xffffffffu, smax = 0u;
+      int dummy;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = tid * 4 + e;
+        const uint32_t key = order_key(s[(int)(((int64_t)i * n_cand) / kSample)]);
+        cand[i] = key;
+        smin = min(smin, key);
+        smax = max(smax, key);
+      }
+      reduce_range(smin, smax, 0, red, smin, smax, dummy);   // its barriers also publish the sample
+      const int sh = top_shift(smin, smax);
+      for (int b = tid; b < kTopBins; b += kThreads) hist[b] = 0;
       __syncthreads();
-      for (int j0 = tid; j0 < n_cand; j0 += kThreads * kHistBatch) {
-        float v[kHistBatch];
 #pragma unroll
-        for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, n_cand - 1)];
+      for (int e = 0; e < 4; ++e) atomicAdd(&hist[(cand[tid * 4 + e] - smin) >> sh], 1);
+      __syncthreads();
+      // T's expected rank in the sample, 1-based from the top
+      const int rr = (int)(((int64_t)ms * kSample + n_cand - 1) / n_cand);
+      const Pick ph = find_bin(hist, kTopBins, max(1, rr - kBandRanks), scan_lds, &sh_pick);
+      const Pick pl = find_bin(hist, kTopBins, min(kSample, rr + kBandRanks), scan_lds, &sh_pick);
+      lo = smin + (pl.bin << sh);
+      hi = (uint64_t)smin + ((uint64_t)(ph.bin + 1u) << sh);
+    }
+    // ---- one pass: count the keys above the band per wave, stage the band
+    if (tid == 0) sh_pos = 0;
+    __syncthreads();
+    int up_count = 0;
+    walk_segment(s, wb, we, [&](int t, const float (&v)[4]) {
 #pragma unroll
-        for (int u = 0; u < kHistBatch; ++u) {
-          const uint32_t key = order_key(v[u]), d = key - kmin;
-          const bool hit = j0 + u * kThreads < n_cand && key >= kfloor && (d & mask) == prefix;
-          const uint64_t bal = __ballot(hit);
-          if (bal) {                              // wave-uniform
-            int base = 0;
-            if (lane == 0) base = atomicAdd(&sh_pos, __popcll(bal));
-            base = __shfl(base, 0, 64);
-            const int at = base + __popcll(bal & ((1ull << lane) - 1ull));
-            if (hit && at < kCandCap) cand[at] = d;
+      for (int e = 0; e < 4; ++e) {
+        const int pos = wb + t * kIter + e * 64 + lane;
+        const uint32_t key = order_key(v[e]);
+        const bool ok = pos < we;
+        const bool up = ok && (uint64_t)key >= hi;
+        const bool in = ok && !up && key >= lo;
+        up_count += up ? 1 : 0;
+        const uint64_t bal = __ballot(in);
+        if (bal) {                              // wave-uniform
+          int base = 0;
+          if (lane == 0) base = atomicAdd(&sh_pos, __popcll(bal));
+          base = __shfl(base, 0, 64);
+          const int at = base + __popcll(bal & below);
+          if (in && at < kCandCap) {
+            cand[at] = key - lo;
+            cpos[at] = pos;
           }
         }
       }
+    });
+    for (int o = 32; o >= 1; o >>= 1) up_count += __shfl_xor(up_count, o, 64);
+    if (lane == 0) wgt[wave] = up_count;
+    __syncthreads();
+    int above = 0;
+    for (int w = 0; w < kWaves; ++w) above += wgt[w];
+    const int banded = sh_pos;
+    if (above < ms && above + banded >= ms && banded <= kCandCap) {
+      // T is the (ms - above)-th largest staged key; the staged keys then
+      // complete the per-wave counts
+      need = ms - above;
+      const uint32_t td = resolve_staged(cand, banded, (uint32_t)min<uint64_t>(hi - lo - 1u, 0xffffffffull), need,
+                                         hist, scan_lds, &sh_pick);
+      T = lo + td;
+      for (int j = tid; j < banded; j += kThreads) {
+        const uint32_t d = cand[j];
+        if (d > td) atomicAdd(&wgt[cpos[j] / seg], 1);
+        else if (d == td) atomicAdd(&weq[cpos[j] / seg], 1);
+      }
+      __syncthreads();
+    } else {
+      // ---- the band missed T or overflowed LDS: radix select on
+      // d = key - (smallest key), then count per wave
+      uint32_t kmin, kmax, prefix, mask;
+      int kabove;
+      need = ms;
+      key_range(s, n_cand, red, kmin, kmax, kabove);
+      // With at least ms keys above -inf the threshold is one of them: those
+      // keys alone are binned (-inf marks what must not be chosen, e.g. the
+      // non-members of the GQA union, and would stretch the range over the
+      // whole key space).  Otherwise every key and the whole range are used.
+      uint32_t kfloor = kNegInfKey + 1u;
+      if (kabove < ms) {
+        kfloor = 0u;
+        kmin = 0u;
+        kmax = 0xffffffffu;
+      }
+      int hi_bit = top_shift(kmin, kmax);
+      histogram<false>(s, nullptr, n_cand, kfloor, kmin, hi_bit, kTopBins, 0u, 0u, hist);
+      Pick pk = find_bin(hist, kTopBins, need, scan_lds, &sh_pick);
+      prefix = pk.bin << hi_bit;
+      mask = ~0u << hi_bit;
+      need = pk.need;
+      const bool staged = pk.count <= kCandCap;
+      if (staged && hi_bit > 0) {
+        // copy the bin's offsets into LDS (order is irrelevant to the threshold)
+        if (tid == 0) sh_pos = 0;
+        __syncthreads();
+        for (int j0 = tid; j0 < n_cand; j0 += kThreads * kHistBatch) {
+          float v[kHistBatch];
+#pragma unroll
+          for (int u = 0; u < kHistBatch; ++u) v[u] = s[min(j0 + u * kThreads, n_cand - 1)];
+#pragma unroll
+          for (int u = 0; u < kHistBatch; ++u) {
+            const uint32_t key = order_key(v[u]), d = key - kmin;
+            const bool hit = j0 + u * kThreads < n_cand && key >= kfloor && (d & mask) == prefix;
+            const uint64_t bal = __ballot(hit);
+            if (bal) {                              // wave-uniform
+              int base = 0;
+              if (lane == 0) base = atomicAdd(&sh_pos, __popcll(bal));
+              base = __shfl(base, 0, 64);
+              const int at = base + __popcll(bal & below);
+              if (hit && at < kCandCap) cand[at] = d;
+            }
+          }
+        }
+        __syncthreads();
+      }
+      // the hi_bit low bits of d, at most kLowBits per pass
+      while (hi_bit > 0) {
+        const int shift = hi_bit > kLowBits ? hi_bit - kLowBits : 0;
+        const int nbins = 1 << (hi_bit - shift);
+        if (staged) histogram<true>(nullptr, cand, pk.count, 0u, 0u, shift, nbins, mask, prefix, hist);
+        else histogram<false>(s, nullptr, n_cand, kfloor, kmin, shift, nbins, mask, prefix, hist);
+        const Pick q = find_bin(hist, nbins, need, scan_lds, &sh_pick);
+        prefix |= q.bin << shift;
+        mask |= ((uint32_t)nbins - 1u) << shift;
+        need = q.need;
+        hi_bit = shift;
+      }
+      T = prefix + kmin;
+      int cg = 0, ce = 0;
+      walk_segment(s, wb, we, [&](int t, const float (&v)[4]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int pos = wb + t * kIter + e * 64 + lane;
+          const uint32_t key = order_key(v[e]);
+          cg += (pos < we && key > T) ? 1 : 0;
+          ce += (pos < we && key == T) ? 1 : 0;
+        }
+      });
+      for (int o = 32; o >= 1; o >>= 1) {
+        cg += __shfl_xor(cg, o, 64);
+        ce += __shfl_xor(ce, o, 64);
+      }
+      if (lane == 0) {
+        wgt[wave] = cg;
+        weq[wave] = ce;
+      }
       __syncthreads();
     }
-    // the hi_bit low bits of d, at most kLowBits per pass
-    while (hi_bit > 0) {
-      const int shift = hi_bit > kLowBits ? hi_bit - kLowBits : 0;
-      const int nbins = 1 << (hi_bit - shift);
-      if (staged) histogram<true>(nullptr, cand, pk.count, 0u, 0u, shift, nbins, mask, prefix, hist);
-      else histogram<false>(s, nullptr, n_cand, kfloor, kmin, shift, nbins, mask, prefix, hist);
-      const Pick q = find_bin(hist, nbins, need, scan_lds, &sh_pick);
-      prefix |= q.bin << shift;
-      mask |= ((uint32_t)nbins - 1u) << shift;
-      need = q.need;
-      hi_bit = shift;
-    }
-    prefix += kmin;   // the threshold key
   } else {
-    prefix = 0xffffffffu;  // nothing is strictly greater; take no ties
-    need = 0;
+    __syncthreads();   // the zeroed counts
   }
-  const uint32_t T = prefix;
 
-  // ---- ordered compaction: keep u > T, and the first `need` keys equal to T.
-  // The kept list index of key j is (keys > T before j) + min(keys == T
-  // before j, need), so one block scan of the packed (> T, == T) counts per
-  // chunk places every key; its evicted index is j minus that.
-  // The scores of chunk c + 1 are loaded before chunk c is scanned, so each
-  // chunk's memory latency hides behind the previous chunk's scan.
-  int run_gt = 0, run_eq = 0;
-  float nxt[kPerThread];
-  auto load_chunk = [&](int base) {
-#pragma unroll
-    for (int e = 0; e < kPerThread; ++e) nxt[e] = s[min(base + tid * kPerThread + e, n_cand - 1)];   // clamped
-  };
-  if (n_cand > 0) load_chunk(0);
-  for (int base = 0; base < n_cand; base += kChunk) {
-    uint32_t u[kPerThread];
-#pragma unroll
-    for (int e = 0; e < kPerThread; ++e) u[e] = order_key(nxt[e]);
-    load_chunk(base + kChunk);   // past the end: re-reads the last score, unused
-    int ngt = 0, neq = 0;
-#pragma unroll
-    for (int e = 0; e < kPerThread; ++e) {
-      const int j = base + tid * kPerThread + e;
-      ngt += (j < n_cand && u[e] > T) ? 1 : 0;
-      neq += (j < n_cand && u[e] == T) ? 1 : 0;
-    }
-    int total;
-    const int pre = block_exclusive_scan(ngt | (neq << 16), scan_lds, total);
-    int gt_b = run_gt + (pre & 0xffff), eq_b = run_eq + (pre >> 16);
-#pragma unroll
-    for (int e = 0; e < kPerThread; ++e) {
-      const int j = base + tid * kPerThread + e;
-      if (j < n_cand) {
-        const int kb = gt_b + min(eq_b, need);
-        const bool keep = u[e] > T || (u[e] == T && eq_b < need);
-        if (keep) {
-          if (kb < ms) kh[kb] = j;
-        } else if (j - kb < n - m) {
-          eh[j - kb] = j;
-        }
-        gt_b += u[e] > T ? 1 : 0;
-        eq_b += u[e] == T ? 1 : 0;
-      }
-    }
-    run_gt += total & 0xffff;
-    run_eq += total >> 16;
+  // ---- compaction.  The kept list index of key j is (keys > T before j) +
+  // min(keys == T before j, need); its evicted index is j minus that.
+  int gt0 = 0, eq0 = 0;
+  for (int w = 0; w < wave; ++w) {
+    gt0 += wgt[w];
+    eq0 += weq[w];
   }
+  walk_segment(s, wb, we, [&](int t, const float (&v)[4]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int pos = wb + t * kIter + e * 64 + lane;
+      const bool ok = pos < we;
+      const uint32_t key = order_key(v[e]);
+      const bool gt = ok && key > T, eq = ok && key == T;
+      const uint64_t bg = __ballot(gt), be = __ballot(eq);
+      const int gb = gt0 + __popcll(bg & below), eb = eq0 + __popcll(be & below);
+      if (ok) {
+        const int kb = gb + min(eb, need);
+        if (gt || (eq && eb < need)) {
+          if (kb < ms) kh[kb] = pos;
+        } else if (pos - kb < n - m) {
+          eh[pos - kb] = pos;
+        }
+      }
+      gt0 += __popcll(bg);
+      eq0 += __popcll(be);
+    }
+  });
   for (int r = tid; r < mr; r += kThreads) kh[ms + r] = n_cand + r;
 }
 
