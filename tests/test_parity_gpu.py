@@ -209,6 +209,26 @@ EDGE = [
 ]
 
 
+MAX_SHAPES = [
+    # the most window rows a KV head may have (G * W = 4096): eight row groups per key chunk
+    (dict(batch=1, H=1, G=8, d=64, n=1024, W=512, dtype="bf16"), None),
+    # the most heads a call may take (batch * H = 65535, the grid's y limit); three heads sampled
+    (dict(batch=65535, H=1, G=1, d=64, n=48, W=8, dtype="fp32"), [(0, 0), (32767, 0), (65534, 0)]),
+]
+
+
+@pytest.mark.parametrize("case,heads", MAX_SHAPES, ids=["max_window_rows", "max_heads"])
+def test_maximum_shapes_stagewise(S, case, heads):
+    """The largest shapes the ABI accepts along its two capped axes, every
+    stage checked against the oracle (on sampled heads for the head cap), plus
+    one decode step."""
+    t = synth.random_case(case["n"] * 3 + case["G"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"], device=DEV)
+    p = make_params(S, case)
+    _, chains = run_stagewise(S, p, t["K"], t["V"], t["Qwin"], heads=heads)
+    run_decode_check(S, p, chains, t["K"], steps=1, seed=7)
+
+
 @pytest.mark.parametrize("case", EDGE, ids=[f"edge{i}" for i in range(len(EDGE))])
 def test_edge_cases_stagewise(S, case):
     case = dict(case)
