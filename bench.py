@@ -723,7 +723,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one MI355X only (every SelKV step is independent per layer and "
+        print("bench.py: measures one MI355X only (every SelKV step is independent per layer and "
               "KV head, and no multi-GPU path is built); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch

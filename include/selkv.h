@@ -60,7 +60,7 @@ typedef enum selkv_status {
   SELKV_OK = 0,
   SELKV_EINVAL = 1,        /* a NULL pointer, a size or parameter out of range */
   SELKV_EDTYPE = 2,        /* kv_dtype is not one of selkv_dtype */
-  SELKV_EUNSUPPORTED = 3,  /* valid request this build does not implement (e.g. head_dim not 64/128) */
+  SELKV_EUNSUPPORTED = 3,  /* valid request the library does not implement (e.g. head_dim not 64/128) */
   SELKV_EALIGN = 4,        /* a pointer violates the alignment rule above */
   SELKV_EWORKSPACE = 5,    /* ws is NULL or ws_bytes is below selkv_workspace_size() */
   SELKV_EHIP = 6           /* a HIP launch returned an error */
