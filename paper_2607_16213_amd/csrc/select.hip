@@ -5,9 +5,10 @@
 // many keys equal to T must be taken (`need`), then compacts.
 //
 // Threshold, usual path (two reads of the scores in all):
-//   sample   4096 keys at evenly spaced positions; a histogram of the sample
-//            over its own key range gives a band of keys around the sample
-//            rank where T is expected (128 sample ranks on either side)
+//   sample   4096 keys at evenly spaced positions; a histogram of the
+//            sampled keys above -inf over their own key range gives a band of
+//            keys around the sample rank where T is expected (128 sample
+//            ranks on either side)
 //   band     one pass over the scores: keys above the band are counted per
 //            wave, keys inside it are staged in LDS with their positions
 //   resolve  when T lies inside the band and the band fits in LDS (nearly
@@ -298,29 +299,39 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* score, in
     uint32_t lo = 0u;
     uint64_t hi = 1ull << 32;
     if (n_cand > kCandCap) {
+      // the sample's keys above -inf span the bins (-inf ranks below them
+      // all and would stretch the range over the whole key space)
       uint32_t smin = 0xffffffffu, smax = 0u;
-      int dummy;
+      int fin = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int i = tid * 4 + e;
         const uint32_t key = order_key(s[(int)(((int64_t)i * n_cand) / kSample)]);
         cand[i] = key;
-        smin = min(smin, key);
-        smax = max(smax, key);
+        if (key > kNegInfKey) {
+          smin = min(smin, key);
+          smax = max(smax, key);
+          ++fin;
+        }
       }
-      reduce_range(smin, smax, 0, red, smin, smax, dummy);   // its barriers also publish the sample
-      const int sh = top_shift(smin, smax);
-      for (int b = tid; b < kTopBins; b += kThreads) hist[b] = 0;
-      __syncthreads();
+      reduce_range(smin, smax, fin, red, smin, smax, fin);   // its barriers also publish the sample
+      if (fin > 0) {
+        const int sh = top_shift(smin, smax);
+        for (int b = tid; b < kTopBins; b += kThreads) hist[b] = 0;
+        __syncthreads();
 #pragma unroll
-      for (int e = 0; e < 4; ++e) atomicAdd(&hist[(cand[tid * 4 + e] - smin) >> sh], 1);
-      __syncthreads();
-      // T's expected rank in the sample, 1-based from the top
-      const int rr = (int)(((int64_t)ms * kSample + n_cand - 1) / n_cand);
-      const Pick ph = find_bin(hist, kTopBins, max(1, rr - kBandRanks), scan_lds, &sh_pick);
-      const Pick pl = find_bin(hist, kTopBins, min(kSample, rr + kBandRanks), scan_lds, &sh_pick);
-      lo = smin + (pl.bin << sh);
-      hi = (uint64_t)smin + ((uint64_t)(ph.bin + 1u) << sh);
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t key = cand[tid * 4 + e];
+          if (key > kNegInfKey) atomicAdd(&hist[(key - smin) >> sh], 1);
+        }
+        __syncthreads();
+        // T's expected rank in the sample, 1-based from the top
+        const int rr = (int)(((int64_t)ms * kSample + n_cand - 1) / n_cand);
+        const Pick ph = find_bin(hist, kTopBins, max(1, min(fin, rr - kBandRanks)), scan_lds, &sh_pick);
+        const Pick pl = find_bin(hist, kTopBins, min(fin, rr + kBandRanks), scan_lds, &sh_pick);
+        lo = smin + (pl.bin << sh);
+        hi = (uint64_t)smin + ((uint64_t)(ph.bin + 1u) << sh);
+      }
     }
     // ---- one pass: count the keys above the band per wave, stage the band
     if (tid == 0) sh_pos = 0;
