@@ -227,7 +227,6 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   // still filling the other
   __shared__ __align__(16) char lds0[Geo::TILE], lds1[Geo::TILE];
   __shared__ __align__(16) float s_inv0[kMT], s_inv1[kMT];   // 1 / ||v_i|| of the tile's kept rows
-  __shared__ __align__(16) float s_off0[kMT], s_off1[kMT];   // 0, or -inf past the last kept slot
   const int64_t head = blockIdx.y;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -271,8 +270,10 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     }
     ixn[slot] = clamp_pos(kh[min((t_begin + tile) * kMT + (tid & (kMT - 1)), m - 1)], n);
   };
-  // past the end the loads re-read the last kept row (masked by s_off), so
-  // every trip issues the same loads
+  // Past the run a trip reads the next run's kept rows (true slots, which
+  // that run reports as well), past the last kept slot it reads kept row
+  // m - 1 again under higher slot numbers: equal values, and ties keep the
+  // lower slot, so nothing needs masking and every trip issues the same loads.
   auto issue_tile = [&](int slot, char* stage) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
@@ -284,14 +285,10 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
     }
     rn = vnh[ixn[slot]];
   };
-  // slots past the run (the trip an odd tile count adds) or past m are masked
-  auto commit_norm = [&](float* sinv, float* soff, int tile) {
-    if (tid < kMT) {
-      sinv[tid] = rn > 0.f ? 1.f / rn : 0.f;
-      soff[tid] = (tile < ntiles && (t_begin + tile) * kMT + tid < m) ? 0.f : kNegInf;
-    }
+  auto commit_norm = [&](float* sinv) {
+    if (tid < kMT) sinv[tid] = rn > 0.f ? 1.f / rn : 0.f;
   };
-  // value = fma(dot, 1 / ||v_i||, off): off = -inf masks slots past the end
+  // value = dot * (1 / ||v_i||)
   // the MFMAs of column block kk + 1 are issued before the epilogue of block
   // kk, so the matrix core and the VALU work on independent data
   auto mfma_block = [&](const char* stage, int kk, f32x4 (&acc)[NRB]) {
@@ -306,17 +303,16 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
       for (int c = 0; c < NCH; ++c) acc[rb] = Mma<bf16_t>::step(bf[c], q[rb][c], acc[rb]);
     }
   };
-  auto epilogue = [&](const float* sinv, const float* soff, int tile, int kk, const f32x4 (&acc)[NRB]) {
+  auto epilogue = [&](const float* sinv, int tile, int kk, const f32x4 (&acc)[NRB]) {
     const int s0 = kk * 16 + grp * 4;
     const f32x4 inv = *reinterpret_cast<const f32x4*>(sinv + s0);
-    const f32x4 off = *reinterpret_cast<const f32x4*>(soff + s0);
     const int slot0 = (t_begin + tile) * kMT + s0;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
-      const float v0 = fmaf(acc[rb][0], inv[0], off[0]);
-      const float v1 = fmaf(acc[rb][1], inv[1], off[1]);
-      const float v2 = fmaf(acc[rb][2], inv[2], off[2]);
-      const float v3 = fmaf(acc[rb][3], inv[3], off[3]);
+      const float v0 = acc[rb][0] * inv[0];
+      const float v1 = acc[rb][1] * inv[1];
+      const float v2 = acc[rb][2] * inv[2];
+      const float v3 = acc[rb][3] * inv[3];
       const float mx = fmaxf(fmaxf(best[rb], v0), fmaxf(fmaxf(v1, v2), v3));
       // slots rise along the stream: only a strictly larger value moves the
       // best, and the lowest of the four slots holding it is taken
@@ -326,23 +322,23 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
       }
     }
   };
-  auto body = [&](const char* stage, const float* sinv, const float* soff, int tile) {
+  auto body = [&](const char* stage, const float* sinv, int tile) {
     f32x4 acc[2][NRB];
     mfma_block(stage, 0, acc[0]);
 #pragma unroll
     for (int kk = 0; kk < kMT / 16; ++kk) {
       if (kk + 1 < kMT / 16) mfma_block(stage, kk + 1, acc[(kk + 1) & 1]);
-      epilogue(sinv, soff, tile, kk, acc[kk & 1]);
+      epilogue(sinv, tile, kk, acc[kk & 1]);
     }
   };
   // trip t: the other stage was released by the last barrier, so tile t+1 is
   // gathered into it while tile t is used; the barrier at the end waits for
   // every load of the trip, issued a whole tile body earlier
-  auto trip = [&](int cur, char* Lc, float* ic, float* oc, char* Ln, float* in_, float* on, int t) {
+  auto trip = [&](int cur, char* Lc, float* ic, char* Ln, float* in_, int t) {
     issue_tile(cur ^ 1, Ln);
     load_pos(cur, t + 2);
-    body(Lc, ic, oc, t);
-    commit_norm(in_, on, t + 1);
+    body(Lc, ic, t);
+    commit_norm(in_);
     __syncthreads();
   };
 
@@ -350,13 +346,13 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   load_pos(0, 0);
   issue_tile(0, lds0);
   load_pos(1, 1);
-  commit_norm(s_inv0, s_off0, 0);
+  commit_norm(s_inv0);
   __syncthreads();
-  // two trips per pass; an odd tile count runs one trip past the end, whose
-  // slots s_off masks to -inf (its loads re-read the last kept row)
+  // two trips per pass; an odd tile count runs one trip past the run (see
+  // issue_tile: its slots need no mask)
   for (int t = 0; t < ntiles; t += 2) {
-    trip(0, lds0, s_inv0, s_off0, lds1, s_inv1, s_off1, t);
-    trip(1, lds1, s_inv1, s_off1, lds0, s_inv0, s_off0, t + 1);
+    trip(0, lds0, s_inv0, lds1, s_inv1, t);
+    trip(1, lds1, s_inv1, lds0, s_inv0, t + 1);
   }
 
   if (!active) return;
