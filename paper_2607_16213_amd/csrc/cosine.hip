@@ -47,6 +47,9 @@ struct MatchArgs {
   int n, m, gate_mode;
   float tau, inv_temp;
   int parts, part_tiles;   // the kept range split into `parts` runs of part_tiles tiles
+  const char* Vk;          // bf16: the kept value rows gathered in slot order, [head][mpad][d]
+  const float* ik;         // and their inverse norms, [head][mpad]
+  int mpad;
 };
 
 // Target and gate of evicted entry e from its best value (dot / ||v_i||) and slot.
@@ -175,14 +178,17 @@ __global__ __launch_bounds__(kThreads) void cosine_match_kernel(MatchArgs a) {
   }
 }
 
-// bf16 variant with the kept rows shared through LDS.  A workgroup holds 256
-// evicted rows (64 per wave, in registers) and streams the head's kept rows
-// in tiles of 64 through two LDS stages that all four waves read.  The tiles
-// are gathered straight into LDS by 16-byte LDS-DMA loads (no register
-// staging): a wave's load fills 1 KB of LDS in lane order, so each lane picks
-// the kept row and 16-byte chunk whose XOR-swizzled place is its own slot.
-// Only the kept positions (one tile ahead) and one norm pass through
-// registers, which keeps the kernel at three waves per SIMD.  The kept tile
+// bf16 variant with the kept rows shared through LDS.  The kept value rows
+// are first copied in slot order into a contiguous block (gather_kept_kernel,
+// with their inverse norms), so the match reads each tile from one base
+// address with no index loads.  A workgroup holds 256 evicted rows (64 per
+// wave, in registers) and streams the head's kept rows in tiles of 64 through
+// two LDS stages that all four waves read.  The tiles go straight into LDS by
+// 16-byte LDS-DMA loads (no register staging): a wave's load fills 1 KB of
+// LDS in lane order, so each lane loads the kept row and 16-byte chunk whose
+// XOR-swizzled place is its own slot.  Only one inverse norm per thread
+// passes through registers, which keeps the kernel at three waves per SIMD
+// with registers to spare.  The kept tile
 // is the MFMA A operand and the evicted rows the B operand, so lane (g, c)
 // receives slots 4g .. 4g+3 of a 16-slot block for evicted row c: its four
 // candidates for one row.  The running argmax takes their maximum with the
@@ -218,6 +224,25 @@ __device__ __forceinline__ void dma_piece(int j, int wave, int lane, int& row, i
   ch = ((p % MGeo<D>::RB) / 16) ^ (row & (MGeo<D>::NCHUNK - 1));
 }
 
+// Kept value rows of every head copied in slot order into Vk, with 1 / ||v||
+// per row (0 for a zero row), for the bf16 match.  Rows m .. mpad - 1 repeat
+// row m - 1, so the match's tiles past the last kept slot need no mask.
+template <int D>
+__global__ __launch_bounds__(kThreads) void gather_kept_kernel(const char* V, const float* vnorm, const int32_t* kept,
+                                                               char* Vk, float* ik, int n, int m, int mpad) {
+  constexpr int RB = D * 2, NCHUNK = RB / 16;
+  const int64_t head = blockIdx.y;
+  const int64_t idx = blockIdx.x * (int64_t)kThreads + threadIdx.x;
+  const int slot = (int)(idx / NCHUNK), ch = (int)(idx % NCHUNK);
+  if (slot >= mpad) return;
+  const int pos = clamp_pos(kept[(size_t)head * m + min(slot, m - 1)], n);
+  store16(Vk + ((size_t)head * mpad + slot) * RB + ch * 16, load16(V + ((size_t)head * n + pos) * RB + ch * 16));
+  if (ch == 0) {
+    const float rn = vnorm[(size_t)head * n + pos];
+    ik[(size_t)head * mpad + slot] = rn > 0.f ? 1.f / rn : 0.f;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   using Geo = MGeo<D>;
@@ -238,8 +263,6 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   const int t_begin = part * a.part_tiles;
   const int t_end = min((m + kMT - 1) / kMT, t_begin + a.part_tiles);
   const char* Vh = a.V + (size_t)head * n * Geo::RB;
-  const float* vnh = a.vnorm + (size_t)head * n;
-  const int32_t* kh = a.kept + (size_t)head * m;
   const int32_t* eh = a.evicted + (size_t)head * ne;
 
   Chunk16 q[NRB][NCH];
@@ -258,35 +281,29 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   }
 
   const int ntiles = max(0, t_end - t_begin);   // tiles of this run; tile t is kept tile t_begin + t
-  int ix[2][LPT];      // kept positions of this thread's DMA rows, one tile ahead
-  int ixn[2];          // kept position of slot tid & (kMT - 1) (its norm), one tile ahead
-  float rn = 0.f;
-  auto load_pos = [&](int slot, int tile) {
-#pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      int row, ch;
-      dma_piece<D>(j, wave, lane, row, ch);
-      ix[slot][j] = clamp_pos(kh[min((t_begin + tile) * kMT + row, m - 1)], n);
-    }
-    ixn[slot] = clamp_pos(kh[min((t_begin + tile) * kMT + (tid & (kMT - 1)), m - 1)], n);
-  };
+  const char* Vkh = a.Vk + (size_t)head * a.mpad * Geo::RB;
+  const float* ikh = a.ik + (size_t)head * a.mpad;
+  float rn = 0.f;   // the inverse norm of slot tid & (kMT - 1) of the tile in flight
   // Past the run a trip reads the next run's kept rows (true slots, which
-  // that run reports as well), past the last kept slot it reads kept row
-  // m - 1 again under higher slot numbers: equal values, and ties keep the
-  // lower slot, so nothing needs masking and every trip issues the same loads.
-  auto issue_tile = [&](int slot, char* stage) {
+  // that run reports as well); past the last kept slot the gathered block
+  // repeats row m - 1 under higher slot numbers: equal values, and ties keep
+  // the lower slot, so nothing needs masking and every trip issues the same
+  // loads.  The block holds two tiles beyond the last (mpad rows), which
+  // covers the trip an odd tile count adds and the load it issues ahead.
+  auto issue_tile = [&](int tile, char* stage) {
+    const char* tb = Vkh + (size_t)(t_begin + tile) * kMT * Geo::RB;
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
       int row, ch;
       dma_piece<D>(j, wave, lane, row, ch);
-      __builtin_amdgcn_global_load_lds(
-          static_cast<const void*>(Vh + (size_t)ix[slot][j] * Geo::RB + ch * 16),
-          (__attribute__((address_space(3))) void*)(stage + (j * kWaves + wave) * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(tb + row * Geo::RB + ch * 16),
+                                       (__attribute__((address_space(3))) void*)(stage + (j * kWaves + wave) * 1024),
+                                       16, 0, 0);
     }
-    rn = vnh[ixn[slot]];
+    rn = ikh[(t_begin + tile) * kMT + (tid & (kMT - 1))];
   };
   auto commit_norm = [&](float* sinv) {
-    if (tid < kMT) sinv[tid] = rn > 0.f ? 1.f / rn : 0.f;
+    if (tid < kMT) sinv[tid] = rn;
   };
   // value = dot * (1 / ||v_i||)
   // the MFMAs of column block kk + 1 are issued before the epilogue of block
@@ -335,17 +352,13 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
   // gathered into it while tile t is used; the barrier at the end waits for
   // every load of the trip, issued a whole tile body earlier
   auto trip = [&](int cur, char* Lc, float* ic, char* Ln, float* in_, int t) {
-    issue_tile(cur ^ 1, Ln);
-    load_pos(cur, t + 2);
+    issue_tile(t + 1, Ln);
     body(Lc, ic, t);
     commit_norm(in_);
     __syncthreads();
   };
 
-  // prologue: tile 0 in stage 0, positions of tile 1
-  load_pos(0, 0);
   issue_tile(0, lds0);
-  load_pos(1, 1);
   commit_norm(s_inv0);
   __syncthreads();
   // two trips per pass; an odd tile count runs one trip past the run (see
@@ -736,7 +749,7 @@ int sort_passes(int m) {
   return (bits + 7) / 8;
 }
 
-GroupPlan plan_group(const Shape& s) {
+GroupPlan plan_group(const Shape& s, int dtype) {
   GroupPlan p{};
   const size_t ne = (size_t)(s.n - s.m);
   const size_t nel = ne > 0 ? ne : 1;
@@ -750,14 +763,23 @@ GroupPlan plan_group(const Shape& s) {
   p.bytes = p.vals_off[1] + align256(nel * (size_t)s.heads * sizeof(int32_t));
   p.passes = sort_passes(s.m);
   p.list_off = p.vals_off[(p.passes - 1) & 1];    // the last pass's values
-  // the match's per-run results come first and are consumed before the grouping starts
+  // the match's scratch (per-run results; bf16: the gathered kept rows and
+  // their inverse norms) comes first and is consumed before the grouping starts
   const int parts = match_parts(s);
   p.match_parts = parts;
+  size_t match_bytes = 0;
   if (parts > 1) {
     p.match_slot_off = align256((size_t)s.heads * parts * ne * sizeof(float));
-    const size_t match_bytes = p.match_slot_off + align256((size_t)s.heads * parts * ne * sizeof(int32_t));
-    p.bytes = std::max(p.bytes, match_bytes);
+    match_bytes = p.match_slot_off + align256((size_t)s.heads * parts * ne * sizeof(int32_t));
   }
+  if (dtype == SELKV_BF16 && ne > 0) {
+    // two tiles past the last: the trip an odd run adds and the load it issues ahead
+    p.match_mpad = ((s.m + kMT - 1) / kMT + 2) * kMT;
+    p.match_vk_off = match_bytes;
+    p.match_ik_off = p.match_vk_off + align256((size_t)s.heads * p.match_mpad * s.d * 2);
+    match_bytes = p.match_ik_off + align256((size_t)s.heads * p.match_mpad * sizeof(float));
+  }
+  p.bytes = std::max(p.bytes, match_bytes);
   return p;
 }
 
@@ -787,6 +809,19 @@ hipError_t launch_cosine_match(const Shape& s, const GroupPlan& gp, int dtype, i
     a.part_tiles = (a.part_tiles + a.parts - 1) / a.parts;
     a.part_best = reinterpret_cast<float*>(ws);
     a.part_slot = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + gp.match_slot_off);
+    a.mpad = gp.match_mpad;
+    char* vk = static_cast<char*>(ws) + gp.match_vk_off;
+    float* ik = reinterpret_cast<float*>(static_cast<char*>(ws) + gp.match_ik_off);
+    a.Vk = vk;
+    a.ik = ik;
+    const int64_t gthreads = (int64_t)a.mpad * (s.d * 2 / 16);
+    const dim3 ggrid((unsigned)((gthreads + kThreads - 1) / kThreads), (unsigned)s.heads);
+    if (s.d == 128)
+      hipLaunchKernelGGL((gather_kept_kernel<128>), ggrid, dim3(kThreads), 0, st, a.V, vnorm, kept, vk, ik, s.n, s.m,
+                         a.mpad);
+    else
+      hipLaunchKernelGGL((gather_kept_kernel<64>), ggrid, dim3(kThreads), 0, st, a.V, vnorm, kept, vk, ik, s.n, s.m,
+                         a.mpad);
     const dim3 grid((unsigned)(row_blocks * a.parts), (unsigned)s.heads);
     if (s.d == 128) hipLaunchKernelGGL((cosine_match_tiled<128>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((cosine_match_tiled<64>), grid, dim3(kThreads), 0, st, a);

@@ -45,6 +45,8 @@ struct GroupPlan {
   int passes;               // 8-bit radix passes over the keys 0 .. m
   int match_parts;          // runs the bf16 match splits the kept range into
   size_t match_slot_off;    // their per-run results: values at 0, slots at match_slot_off
+  int match_mpad;           // bf16: rows per head of the gathered kept value block
+  size_t match_vk_off, match_ik_off;   // the gathered block and its inverse norms
 };
 
 // Workspace of the GQA union mode: flags, mean keys and the shared set per
@@ -56,7 +58,7 @@ struct UnionPlan {
 
 ScorePlan plan_score(const Shape& s, int dtype);
 UnionPlan plan_union(const Shape& s);
-GroupPlan plan_group(const Shape& s);
+GroupPlan plan_group(const Shape& s, int dtype);
 DecodePlan plan_decode(int64_t heads, int cache_len, int d, int G);
 // bytes that cover plan_decode(heads, L, d, G).bytes for every L <= capacity
 size_t decode_workspace_bound(int64_t heads, int capacity, int d, int G);

@@ -77,7 +77,7 @@ size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 // merge and bias workspace: the bucket offsets under the bucket routings,
 // the grouping by target slot under full-cosine routing
 size_t merge_bytes(const selkv_params* p, const Shape& s) {
-  return p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s).bytes : bucket_offsets_bytes(s);
+  return p->route_mode == SELKV_ROUTE_FULL_COSINE ? plan_group(s, p->kv_dtype).bytes : bucket_offsets_bytes(s);
 }
 
 // co-attention routing workspace: the score pass's row statistics, then the bucket offsets
@@ -178,7 +178,7 @@ selkv_status run_merge(const selkv_params* p, const Shape& s, const void* K, con
                                           p->alpha, raw, stream));
   }
   // all-pairs routing: match, group by target slot, merge per slot
-  const GroupPlan gp = plan_group(s);
+  const GroupPlan gp = plan_group(s, p->kv_dtype);
   e = launch_cosine_match(s, gp, p->kv_dtype, p->gate_mode, p->gate_threshold, p->gate_temperature, V, vnorm,
                           kept_idx, evicted_idx, target, gate, ws, stream);
   if (e != hipSuccess) return SELKV_EHIP;
@@ -360,7 +360,7 @@ SELKV_API selkv_status selkv_bias(const selkv_params* p, const float* attn, cons
   float* dst = uni ? reinterpret_cast<float*>(static_cast<char*>(ws) + round256(base)) : bias;
   hipError_t e;
   if (p->route_mode == SELKV_ROUTE_FULL_COSINE) {
-    const GroupPlan gp = plan_group(s);
+    const GroupPlan gp = plan_group(s, p->kv_dtype);
     e = launch_group(s, gp, target, ws, stream);
     if (e != hipSuccess) return SELKV_EHIP;
     e = launch_group_merge(s, gp, p->kv_dtype, nullptr, nullptr, attn, kept_idx, evicted_idx, gate, ws, nullptr,
