@@ -375,7 +375,8 @@ FULLCOS = [
     dict(batch=1, H=1, G=2, d=64, n=300, W=32, dtype="bf16", budget_ratio=1.0),       # nothing evicted
     dict(batch=1, H=1, G=2, d=64, n=100, W=8, dtype="fp32", budget_ratio=0.05),       # m < 16: one partial tile
     dict(batch=1, H=1, G=2, d=64, n=20000, W=32, dtype="bf16", budget_ratio=0.9),     # m > 16384 cursor slots
-    # the kept range split into runs of 9 tiles (odd: each run's extra trip is masked), merged in slot order
+    # the kept range split into runs of 9 tiles (odd: each run's extra trip reads the next run's first tile,
+    # the last run's reads the repeated last kept row), merged in slot order
     dict(batch=1, H=2, G=2, d=128, n=4400, W=32, dtype="bf16", budget_ratio=0.5),
     dict(batch=2, H=1, G=4, d=64, n=9000, W=32, dtype="bf16", budget_ratio=0.3, gate_mode=2),
 ]
