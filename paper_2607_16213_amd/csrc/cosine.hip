@@ -333,8 +333,9 @@ __global__ __launch_bounds__(kThreads, 3) void cosine_match_tiled(MatchArgs a) {
       const float mx = fmaxf(fmaxf(best[rb], v0), fmaxf(fmaxf(v1, v2), v3));
       // slots rise along the stream: only a strictly larger value moves the
       // best, and the lowest of the four slots holding it is taken
-      if (mx > best[rb]) {
-        bidx[rb] = v0 == mx ? slot0 : v1 == mx ? slot0 + 1 : v2 == mx ? slot0 + 2 : slot0 + 3;
+      if (mx > best[rb]) {   // the lowest of the four equal to mx: one find-first-set on their flags
+        const uint32_t eq = (v0 == mx ? 1u : 0u) | (v1 == mx ? 2u : 0u) | (v2 == mx ? 4u : 0u) | 8u;
+        bidx[rb] = slot0 + (int)__builtin_ctz(eq);
         best[rb] = mx;
       }
     }
