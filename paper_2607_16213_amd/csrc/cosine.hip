@@ -569,15 +569,30 @@ __global__ __launch_bounds__(kThreads) void sort_offsets_kernel(const int32_t* k
   off[(size_t)head * (m + 1) + s] = lo;
 }
 
+// The listed tokens' positions and Eq. 5 weights g_j * a_j, in list order:
+// gathered once here so the merge reads them without a chain of dependent
+// lookups (token index -> position -> attention) per slot.
+__global__ __launch_bounds__(kThreads) void group_payload_kernel(const int32_t* list, const int32_t* evicted,
+                                                                 const float* gate, const float* attn,
+                                                                 int32_t* lpos, float* lw, int n, int ne) {
+  const int64_t head = blockIdx.y;
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i >= ne) return;
+  const size_t o = (size_t)head * ne + i;
+  const int e = (int)min((uint32_t)list[o], (uint32_t)(ne - 1));
+  const int jp = clamp_pos(evicted[(size_t)head * ne + e], n);
+  lpos[o] = jp;
+  lw[o] = weight_rn(gate[(size_t)head * ne + e], attn[(size_t)head * n + jp]);
+}
+
 struct GroupMergeArgs {
   const char* K;
   const char* V;
   const float* attn;
   const int32_t* kept;
-  const int32_t* evicted;
-  const float* gate;
   const int32_t* off;
-  const int32_t* list;
+  const int32_t* lpos;   // per list entry: the token's position
+  const float* lw;       // and its weight g * a
   char* K_out;
   char* V_out;
   float* bias;
@@ -586,129 +601,163 @@ struct GroupMergeArgs {
   int raw;   // bias mode: write wsum / a_s (R - 1) instead of alpha * ln R
 };
 
-// One wave per kept slot: Eq. 5 (and the Eq. 6 bias when `bias` is set) over
-// the slot's ascending list; lane group q takes list entries q, q+4, ...
+// Eq. 5 (and the Eq. 6 bias when `bias` is set) per kept slot, kSlotsPerWave
+// consecutive slots per wave: their lists are contiguous in the sorted order,
+// so the wave walks the combined range [off[s0], off[s0 + kSlotsPerWave]) in
+// chunks of 64 entries.  Entry p of the range (counted from its start) goes to
+// lane group p % 4, which adds it to its running sums of the entry's slot;
+// the four lane groups' sums of a slot combine as (g0 + g1) + (g2 + g3), and
+// lane group k writes slot s0 + k.  A slot's sums are thus formed in one
+// fixed order, the same in the values pass and the bias pass, and a long list
+// still spreads over all four lane groups.
 // MK (values mode only): keys merged with the value weights instead of gathered
+constexpr int kSlotsPerWave = 4;   // one per lane group
+
 template <typename T, int D, bool VALUES, bool MK>
 __global__ __launch_bounds__(kThreads) void group_merge_kernel(GroupMergeArgs a) {
   constexpr int E = Slice<T, D>::kElems;
   constexpr int RB = D * (int)sizeof(T);
+  constexpr int SPW = kSlotsPerWave;
+  constexpr int EK = MK ? E : 1;
   const int64_t head = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int s = blockIdx.x * kWaves + wave;
+  const int s0 = (blockIdx.x * kWaves + wave) * SPW;
   const int n = a.n, m = a.m, ne = n - m;
-  if (s >= m) return;
+  if (s0 >= m) return;
   const int32_t* kh = a.kept + (size_t)head * m;
-  const int32_t* eh = a.evicted + (size_t)head * ne;
-  const float* gh = a.gate + (size_t)head * ne;
   const int32_t* oh = a.off + (size_t)head * (m + 1);
-  const int32_t* lh = a.list + (size_t)head * ne;
+  const int32_t* ph = a.lpos + (size_t)head * ne;
+  const float* wh = a.lw + (size_t)head * ne;
   const float* ah = a.attn + (size_t)head * n;
-  const int pos = clamp_pos(kh[s], n);
-  const int l0 = oh[s], l1 = oh[s + 1];
+  // list bounds of the wave's slots; slots past m have empty lists, and with
+  // nothing evicted there are no lists (the grouping wrote no offsets)
+  int L[SPW + 1];
+#pragma unroll
+  for (int k = 0; k <= SPW; ++k) L[k] = ne > 0 ? oh[min(s0 + k, m)] : 0;
+  // lane group grp owns slot s0 + grp: its rows are loaded ahead of the walk
+  const int my = s0 + grp;
+  const int pos = clamp_pos(kh[min(my, m - 1)], n);
+  RawSlice<T, D> kr, vr;
+  if constexpr (VALUES) {
+    kr.load(a.K + ((size_t)head * n + pos) * RB, col);
+    vr.load(a.V + ((size_t)head * n + pos) * RB, col);
+  }
   const float a_s = ah[pos];
 
-  float acc[E], kacc[MK ? E : 1];
+  float acc[SPW][VALUES ? E : 1], kacc[SPW][EK], wsum[SPW];
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  for (int k = 0; k < SPW; ++k) {
 #pragma unroll
-  for (int e = 0; e < (MK ? E : 1); ++e) kacc[e] = 0.f;
-  float wsum = 0.f;
-  for (int lb = l0; lb < l1; lb += 64) {
-    // lane-parallel metadata of up to 64 list entries
+    for (int e = 0; e < (VALUES ? E : 1); ++e) acc[k][e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EK; ++e) kacc[k][e] = 0.f;
+    wsum[k] = 0.f;
+  }
+  for (int lb = L[0]; lb < L[SPW]; lb += 64) {
+    // lane-parallel metadata of up to 64 entries: position, weight, slot
     const int li = lb + lane;
-    int jp = 0;
+    int jp = 0, sk = 0;
     float w = 0.f;
-    if (li < l1) {
-      const int e = lh[li];
-      jp = clamp_pos(eh[e], n);
-      w = weight_rn(gh[e], ah[jp]);
+    if (li < L[SPW]) {
+      jp = ph[li];
+      w = wh[li];
+#pragma unroll
+      for (int k = 1; k < SPW; ++k) sk += li >= L[k] ? 1 : 0;
     }
-    const int cnt = min(64, l1 - lb);
-    if (!VALUES) {
-      wsum = seg_sum_add(wsum, w, lane);   // the running group sums, in the values pass's order
-      continue;
-    }
+    const int cnt = min(64, L[SPW] - lb);
     constexpr int kBatch = 4;
     for (int ib0 = 0; ib0 < cnt; ib0 += 4 * kBatch) {
-      int jj[kBatch];
+      int jj[kBatch], kk[kBatch];
       float wv[kBatch];
-      RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
+      RawSlice<T, D> vv[VALUES ? kBatch : 1], kre[MK ? kBatch : 1];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = ib0 + 4 * u + grp;
         const int src = i < cnt ? i : 0;
-        // both shuffles run on every lane: a shuffle under a lane-dependent
+        // the shuffles run on every lane: a shuffle under a lane-dependent
         // condition would read inactive source lanes
         jj[u] = __shfl(jp, src, 64);
         wv[u] = __shfl(w, src, 64);
+        kk[u] = __shfl(sk, src, 64);
       }
+      if constexpr (VALUES) {
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) vr[u].load(a.V + ((size_t)head * n + jj[u]) * RB, col);
+        for (int u = 0; u < kBatch; ++u) vv[u].load(a.V + ((size_t)head * n + jj[u]) * RB, col);
+      }
       if constexpr (MK) {
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) kre[u].load(a.K + ((size_t)head * n + jj[u]) * RB, col);
       }
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int i = ib0 + 4 * u + grp;
-        if (i < cnt) {
+        if (ib0 + 4 * u + grp < cnt) {
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[e] = fmaf(wv[u], vr[u].get(e), acc[e]);
-          if constexpr (MK) {
+          for (int k = 0; k < SPW; ++k) {
+            const bool hit = kk[u] == k;
+            if constexpr (VALUES) {
 #pragma unroll
-            for (int e = 0; e < E; ++e) kacc[e] = fmaf(wv[u], kre[u].get(e), kacc[e]);
+              for (int e = 0; e < E; ++e) acc[k][e] = hit ? fmaf(wv[u], vv[u].get(e), acc[k][e]) : acc[k][e];
+            }
+            if constexpr (MK) {
+#pragma unroll
+              for (int e = 0; e < E; ++e) kacc[k][e] = hit ? fmaf(wv[u], kre[u].get(e), kacc[k][e]) : kacc[k][e];
+            }
+            wsum[k] = hit ? wsum[k] + wv[u] : wsum[k];
           }
-          wsum += wv[u];
         }
       }
     }
   }
-  if (!VALUES) {
-    wsum = seg_sum_total(wsum);
-    if (lane == 0) a.bias[(size_t)head * m + s] = ratio_bias(wsum, a_s, a.alpha, a.raw != 0);
-    return;
-  }
+  // (g0 + g1) + (g2 + g3) on every lane, then lane group grp keeps its slot's sums
+  float mw = 0.f, mv[VALUES ? E : 1], mk[EK];
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    acc[e] += xor_shfl(acc[e], 16);
-    acc[e] += xor_shfl(acc[e], 32);
-  }
-  if constexpr (MK) {
+  for (int e = 0; e < (VALUES ? E : 1); ++e) mv[e] = 0.f;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      kacc[e] += xor_shfl(kacc[e], 16);
-      kacc[e] += xor_shfl(kacc[e], 32);
+  for (int e = 0; e < EK; ++e) mk[e] = 0.f;
+#pragma unroll
+  for (int k = 0; k < SPW; ++k) {
+    wsum[k] += xor_shfl(wsum[k], 16);
+    wsum[k] += xor_shfl(wsum[k], 32);
+    mw = grp == k ? wsum[k] : mw;
+    if constexpr (VALUES) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        acc[k][e] += xor_shfl(acc[k][e], 16);
+        acc[k][e] += xor_shfl(acc[k][e], 32);
+        mv[e] = grp == k ? acc[k][e] : mv[e];
+      }
+    }
+    if constexpr (MK) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        kacc[k][e] += xor_shfl(kacc[k][e], 16);
+        kacc[k][e] += xor_shfl(kacc[k][e], 32);
+        mk[e] = grp == k ? kacc[k][e] : mk[e];
+      }
     }
   }
-  wsum += xor_shfl(wsum, 16);
-  wsum += xor_shfl(wsum, 32);
-  // fused call: the Eq. 6 bias of the slot from the same absorbed mass
-  if (a.bias != nullptr && lane == 0) a.bias[(size_t)head * m + s] = ratio_bias(wsum, a_s, a.alpha, a.raw != 0);
-  if (grp == 0) {
-    const char* krow = a.K + ((size_t)head * n + pos) * RB;
-    const char* vrow = a.V + ((size_t)head * n + pos) * RB;
-    RawSlice<T, D> kr, vr;
-    kr.load(krow, col);
-    vr.load(vrow, col);
-    if (wsum > 0.f) {
-      const float den = a_s + wsum;
-      RawSlice<T, D> mv;
+  if (my >= m) return;
+  // the Eq. 6 bias of the slot from the same absorbed mass (fused call, or the bias pass)
+  if (a.bias != nullptr && col == 0) a.bias[(size_t)head * m + my] = ratio_bias(mw, a_s, a.alpha, a.raw != 0);
+  if constexpr (VALUES) {
+    if (mw > 0.f) {
+      const float den = a_s + mw;
+      RawSlice<T, D> ov;
 #pragma unroll
-      for (int e = 0; e < E; ++e) mv.put(e, fmaf(a_s, vr.get(e), acc[e]) / den);
-      mv.store(a.V_out + ((size_t)head * m + s) * RB, col);
+      for (int e = 0; e < E; ++e) ov.put(e, fmaf(a_s, vr.get(e), mv[e]) / den);
+      ov.store(a.V_out + ((size_t)head * m + my) * RB, col);
       if constexpr (MK) {
-        RawSlice<T, D> mk;
+        RawSlice<T, D> ok;
 #pragma unroll
-        for (int e = 0; e < E; ++e) mk.put(e, fmaf(a_s, kr.get(e), kacc[e]) / den);
-        mk.store(a.K_out + ((size_t)head * m + s) * RB, col);
+        for (int e = 0; e < E; ++e) ok.put(e, fmaf(a_s, kr.get(e), mk[e]) / den);
+        ok.store(a.K_out + ((size_t)head * m + my) * RB, col);
       } else {
-        kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
+        kr.store(a.K_out + ((size_t)head * m + my) * RB, col);
       }
     } else {
-      kr.store(a.K_out + ((size_t)head * m + s) * RB, col);
-      vr.store(a.V_out + ((size_t)head * m + s) * RB, col);
+      kr.store(a.K_out + ((size_t)head * m + my) * RB, col);
+      vr.store(a.V_out + ((size_t)head * m + my) * RB, col);
     }
   }
 }
@@ -865,18 +914,25 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
 
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
-                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
+                              void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
                               bool merge_keys, hipStream_t st) {
-  const char* w = static_cast<const char*>(ws);
+  char* w = static_cast<char*>(ws);
   GroupMergeArgs a{};
   a.K = static_cast<const char*>(K);
   a.V = static_cast<const char*>(V);
   a.attn = attn;
   a.kept = kept;
-  a.evicted = evicted;
-  a.gate = gate;
   a.off = reinterpret_cast<const int32_t*>(w + p.off_off);
-  a.list = reinterpret_cast<const int32_t*>(w + p.list_off);
+  // the payload goes to the sort buffers the last pass read (free once it ran)
+  int32_t* lpos = reinterpret_cast<int32_t*>(w + p.vals_off[p.passes & 1]);
+  float* lw = reinterpret_cast<float*>(w + p.keys_off[p.passes & 1]);
+  a.lpos = lpos;
+  a.lw = lw;
+  const int ne = s.n - s.m;
+  if (ne > 0)
+    hipLaunchKernelGGL(group_payload_kernel, dim3((unsigned)((ne + kThreads - 1) / kThreads), (unsigned)s.heads),
+                       dim3(kThreads), 0, st, reinterpret_cast<const int32_t*>(w + p.list_off), evicted, gate, attn,
+                       lpos, lw, s.n, ne);
   a.K_out = static_cast<char*>(K_out);
   a.V_out = static_cast<char*>(V_out);
   a.bias = bias;
@@ -884,7 +940,8 @@ hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, con
   a.m = s.m;
   a.alpha = alpha;
   a.raw = raw ? 1 : 0;
-  const dim3 grid((s.m + kWaves - 1) / kWaves, (unsigned)s.heads);
+  const int waves = (s.m + kSlotsPerWave - 1) / kSlotsPerWave;
+  const dim3 grid((waves + kWaves - 1) / kWaves, (unsigned)s.heads);
   const bool values = V_out != nullptr;   // else the bias pass alone
 #define SELKV_GM(T, D)                                                                                     \
   do {                                                                                                     \

@@ -100,7 +100,7 @@ hipError_t launch_group(const Shape& s, const GroupPlan& p, const int32_t* targe
 // values pass when V_out is set (bias, when also set, from the same sums); bias pass alone otherwise
 hipError_t launch_group_merge(const Shape& s, const GroupPlan& p, int dtype, const void* K, const void* V,
                               const float* attn, const int32_t* kept, const int32_t* evicted, const float* gate,
-                              const void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
+                              void* ws, void* K_out, void* V_out, float* bias, float alpha, bool raw,
                               bool merge_keys, hipStream_t st);
 hipError_t launch_union_select(const Shape& s, const UnionPlan& p, const float* score, int32_t* kept,
                                int32_t* evicted, void* ws, hipStream_t st);
