@@ -420,7 +420,12 @@ __global__ __launch_bounds__(kThreads) void match_parts_kernel(MatchArgs a) {
 }
 
 
-// In place: cnt[head][0..m] becomes the exclusive prefix sum (off[m] = total).
+// In place: cnt[head][0..m] becomes the exclusive prefix sum (cnt[m] = total).
+// Rounds of 1024 x kScanRun entries: each thread loads its kScanRun
+// consecutive entries at once and scans them in order, the workgroup scans
+// the thread totals, so a round costs one load latency.
+constexpr int kScanRun = 8;
+
 __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
   const int64_t head = blockIdx.x;
   int32_t* c = cnt + (size_t)head * (m + 1);
@@ -429,10 +434,19 @@ __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) s_run = 0;
   __syncthreads();
-  for (int base = 0; base <= m; base += 1024) {
-    const int i = base + tid;
-    const int v = (i < m) ? c[i] : 0;
-    const int incl = wave_inclusive_scan(v, lane);
+  for (int base = 0; base <= m; base += 1024 * kScanRun) {
+    const int i0 = base + tid * kScanRun;
+    int v[kScanRun];
+#pragma unroll
+    for (int r = 0; r < kScanRun; ++r) v[r] = (i0 + r < m) ? c[i0 + r] : 0;
+    int t = 0;
+#pragma unroll
+    for (int r = 0; r < kScanRun; ++r) {   // exclusive within the thread's run
+      const int x = v[r];
+      v[r] = t;
+      t += x;
+    }
+    const int incl = wave_inclusive_scan(t, lane);
     if (lane == 63) s_w[wave] = incl;
     __syncthreads();
     int woff = 0;
@@ -440,7 +454,10 @@ __global__ __launch_bounds__(1024) void group_scan_kernel(int32_t* cnt, int m) {
     int total = 0;
     for (int w = 0; w < 16; ++w) total += s_w[w];
     const int run = s_run;
-    if (i <= m) c[i] = run + woff + incl - v;
+    const int pre = run + woff + incl - t;
+#pragma unroll
+    for (int r = 0; r < kScanRun; ++r)
+      if (i0 + r <= m) c[i0 + r] = pre + v[r];
     __syncthreads();
     if (tid == 0) s_run = run + total;
     __syncthreads();
