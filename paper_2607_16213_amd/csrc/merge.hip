@@ -308,10 +308,16 @@ __global__ __launch_bounds__(kThreads) void merge_bucket_kernel(MergeArgs a) {
 #pragma unroll
   for (int e = 0; e < (MK ? E : 1); ++e) kacc[e] = 0.f;
   float wsum = 0.f;
+  // a bucket that keeps nothing (the wave agrees on tslot): its evicted tokens
+  // go nowhere with gate 0 and their rows are not read
+  if (tslot < 0 && lane < ne) {
+    store_u32off(th, (uint32_t)(e0 + lane), -1);
+    store_u32off(gh, (uint32_t)(e0 + lane), 0.f);
+  }
   // evicted rows, kBatch per lane group with their loads issued together;
   // lane group q takes entries 4u + q (uniform trip count, masked)
   constexpr int kBatch = 4;
-  for (int ib0 = 0; ib0 < ne; ib0 += 4 * kBatch) {
+  for (int ib0 = 0; ib0 < (tslot >= 0 ? ne : 0); ib0 += 4 * kBatch) {
     int jj[kBatch];
     float ajv[kBatch], vnjv[kBatch];
     RawSlice<T, D> vr[kBatch], kre[MK ? kBatch : 1];
