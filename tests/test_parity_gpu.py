@@ -1178,6 +1178,46 @@ def test_merge_bias_fused_equals_merge_then_bias(S, case):
             record("fused_vs_oracle", f"{case} {kw} b{b} h{h}", **counts)
 
 
+# ------------------------------------------------------------------ workspaces need no initialisation
+DIRTY = FUSED + [
+    dict(batch=1, H=2, G=2, d=64, n=300, W=16, dtype="bf16", route_mode="full_cosine", budget_ratio=1.0),
+    dict(batch=1, H=2, G=2, d=64, n=300, W=16, dtype="fp32", select_mode="union", budget_ratio=1.0),
+]
+
+
+@pytest.mark.parametrize("case", DIRTY, ids=[f"dirty{i}" for i in range(len(DIRTY))])
+def test_compression_workspaces_need_no_zero_fill(S, case):
+    """The score, select, route and merge workspaces are scratch the library
+    writes before it reads: filled with seeded random bytes instead of zeros,
+    every output of the compression (fused and merge-then-bias) is bit for bit
+    the same, in every routing, selection and key mode and with nothing
+    evicted (rho = 1, where the full-cosine grouping writes no offsets)."""
+    case = dict(case)
+    kw = {k: case.pop(k) for k in list(case) if k not in ("batch", "H", "G", "d", "n", "W", "dtype")}
+    t = synth.random_case(case["n"] * 11 + 3, batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
+                          head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"],
+                          clusters=6, device=DEV)
+    p = make_params(S, case, **kw)
+    print(f"dirty workspace case {case} {kw}", flush=True)
+    gen = torch.Generator(device="cpu").manual_seed(case["n"])
+    for fused in (True, False):
+        comp = S.Compressor(p, DEV)
+        comp.run(t["K"], t["V"], t["Qwin"], fused=fused)
+        torch.cuda.synchronize()
+        clean = {k: v.clone() for k, v in comp.outputs().items()}
+        for ws in (comp.ws_score, comp.ws_select, comp.ws_merge, comp.ws_route):
+            if ws is not None:
+                ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, generator=gen))
+        comp.run(t["K"], t["V"], t["Qwin"], fused=fused)
+        torch.cuda.synchronize()
+        for k, v in comp.outputs().items():
+            a, b = clean[k], v
+            if a.is_floating_point():
+                a, b = a.view(torch.int16 if a.element_size() == 2 else torch.int32), \
+                    b.view(torch.int16 if b.element_size() == 2 else torch.int32)
+            assert torch.equal(a, b), f"{k} differs after a dirty workspace (fused={fused})"
+
+
 # ------------------------------------------------------------------ selection: the threshold's bin
 def _select_case(rng, kind):
     """(n, m, scores [2, n - 16] fp32) for a selection whose threshold falls
