@@ -11,7 +11,8 @@
  *    library never allocates, frees or retains memory, and keeps no state
  *    between calls.  Scratch memory is passed in as `ws` / `ws_bytes`,
  *    sized by selkv_workspace_size(); a call whose workspace size is 0 may
- *    pass NULL.
+ *    pass NULL.  A workspace needs no initialisation: every call writes the
+ *    scratch it reads, so its contents on entry never change a result.
  *  - Tensors are dense, row-major, contiguous.  "B" is any leading batch of
  *    independent caches: sequences, or sequences x layers when a whole
  *    model's caches are stored back to back, since every step is

@@ -133,7 +133,7 @@ def workspace_bytes(p: Params, call: int, cache_len: int = 0) -> int:
 
 
 def workspace(p: Params, call: int, device, cache_len: int = 0) -> torch.Tensor:
-    """Scratch for `call`, zero-filled (the decode workspace must start at zero)."""
+    """Scratch for `call` (zero-filled for tidiness; no call needs it initialised)."""
     nbytes = workspace_bytes(p, call, cache_len)
     return torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=device)
 
