@@ -265,7 +265,7 @@ def cpu_baseline(job, n_heads, dev, extra_jobs=()):
                 O.decode(q, r["k_out"][None], r["v_out"][None], r["bias"][None], w.group, 1 / math.sqrt(w.head_dim))
                 t_dec += time.perf_counter() - t0
                 nd += 1
-    # slices over the host cores: the machine's CPU share, at most 16 processes, each
+    # slices over the host cores: at most 16 processes (the host's CPU share), each
     # taking two slices; the slices are staged in files and the workers have
     # imported the oracle before the timed region starts
     import shutil
