@@ -1417,7 +1417,9 @@ def test_full_cosine_full_size_sampled(S):
     sampled evicted rows of two heads the float64 cosine argmax over all
     kept rows (lowest slot on ties) must be the GPU's target, except where
     the two cosines lie within 1e-6 of each other relative (counted); gates
-    follow the chosen target's cosine."""
+    follow the chosen target's cosine.  Every kept slot of those heads is
+    then checked: keys gathered bit for bit, merged values (Eq. 5) and
+    biases (Eq. 6) against float64 on the GPU's own targets and gates."""
     w = synth.WORKLOADS["ctx100k"]
     t = synth.make_layer(w, 0, DEV)
     K, V, Q = t["K"], t["V"], t["Qwin"]
@@ -1449,6 +1451,26 @@ def test_full_cosine_full_size_sampled(S):
                 assert c_got >= c_ref - NEAR_TIE * abs(c_ref), f"head {h} row {ev[rows[r]]}: {c_got!r} vs {c_ref!r}"
                 ties += 1
             assert abs(g[r] - min(1.0, max(0.0, c_got))) <= GATE_ATOL, f"gate head {h} row {ev[rows[r]]}"
+    # the grouping and the segmented merge at this size: every kept slot of the two heads against
+    # the float64 Eq. 5 and Eq. 6 on the GPU's own targets and gates (so no near-tie can differ)
+    bias = torch.empty_like(comp.bias)
+    S.bias(pf, comp.attn, comp.kept, comp.evicted, target, gate, bias, S.workspace(pf, S.CALL_BIAS, DEV))
+    torch.cuda.synchronize()
+    alpha = float(np.float32(pf.alpha))
+    for h in (0, 5):
+        kept = comp.kept[0, h].cpu().numpy()
+        ev = comp.evicted[0, h].cpu().numpy()
+        a = np64(comp.attn[0, h])
+        tg = target[0, h].cpu().numpy()
+        g = np64(gate[0, h])
+        _, v_ref, _ = O.merge(np64(K[0, h]), np64(V[0, h]), a, kept, ev, tg, g)
+        assert torch.equal(K_out[0, h].cpu(), K[0, h].cpu()[torch.as_tensor(kept, dtype=torch.long)]), f"K_out head {h}"
+        assert_close_rows(np64(V_out[0, h]), v_ref, TOL["bf16"], f"V_out head {h}")
+        b_ref = O.ratio_bias(a, kept, ev, tg, g, alpha)
+        err = np.abs(np64(bias[0, h]) - b_ref).max()
+        assert err <= alpha * TOL["fp32"], f"bias head {h} err {err:.3e}"
+        absorbed = np.unique(tg[(tg >= 0) & (g * a[ev] > 0)])
+        assert (np64(bias[0, h])[np.setdiff1d(np.arange(len(kept)), absorbed)] == 0).all(), "bias 0 where R = 1"
     record("full_cosine_full_size_sampled", "ctx100k layer 0 heads 0,5 (1024 rows)", route_ties=ties)
 
 
