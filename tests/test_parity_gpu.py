@@ -1482,7 +1482,9 @@ def test_coattn_full_size_sampled(S):
     the kept tokens of the token's bucket of sum_r A[r, j] A[r, i] (A over
     all 4 x 32 window rows, lowest position on ties) must be the GPU's
     target, except within 1e-6 relative of each other; -1 exactly where the
-    bucket keeps nothing; gates follow the chosen target's value cosine."""
+    bucket keeps nothing; gates follow the chosen target's value cosine.
+    Every kept slot of those heads: keys gathered bit for bit, merged values
+    and biases against float64 on the GPU's own targets and gates."""
     w = synth.WORKLOADS["ctx100k"]
     t = synth.make_layer(w, 0, DEV)
     K, V, Q = t["K"], t["V"], t["Qwin"]
@@ -1521,6 +1523,16 @@ def test_coattn_full_size_sampled(S):
             g_ref = O.gate(V64, kept, ev[r:r + 1], tg[r:r + 1], GATE[p.gate_mode], float(np.float32(p.gate_threshold)),
                            float(np.float32(p.gate_temperature)))[0]
             assert abs(g[r] - g_ref) <= GATE_ATOL, f"gate head {h} evicted {j}"
+        # the merge per target at this size: every kept slot against the float64 Eq. 5 / Eq. 6 on
+        # the GPU's own attention, targets and gates
+        a = np64(comp.attn[0, h])
+        ga = np64(comp.gate[0, h])
+        _, v_ref, _ = O.merge(K64, V64, a, kept, ev, tg, ga)
+        assert torch.equal(comp.K_out[0, h].cpu(), K[0, h].cpu()[torch.as_tensor(kept, dtype=torch.long)])
+        assert_close_rows(np64(comp.V_out[0, h]), v_ref, TOL["bf16"], f"V_out head {h}")
+        alpha = float(np.float32(p.alpha))
+        err = np.abs(np64(comp.bias[0, h]) - O.ratio_bias(a, kept, ev, tg, ga, alpha)).max()
+        assert err <= alpha * TOL["fp32"], f"bias head {h} err {err:.3e}"
     record("coattn_full_size_sampled", "ctx100k layer 0 heads 2,7 (1024 rows)", route_ties=ties, unrouted=unrouted)
 
 
