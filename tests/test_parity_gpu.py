@@ -670,6 +670,23 @@ def test_gqa_union_end_to_end_llama_layer(S):
     record("gqa_union_end_to_end", "llama_layer", **counts)
 
 
+def test_gqa_union_full_size(S):
+    """Union-mode compression at the bench's layer size (one ctx100k layer:
+    8 KV heads x 102400 tokens, 25600 kept) on the GPU against the oracle's
+    union mode: the shared kept set equal to the oracle's but for near-ties
+    of the float64 trim mean (counted), then every head's targets, gates,
+    merged values and the head-averaged bias to their bars."""
+    w = synth.WORKLOADS["ctx100k"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w), select_mode="union")
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    kept = comp.kept[0].cpu().numpy()
+    assert (kept == kept[0]).all(), "all KV heads share one kept set"
+    counts = union_oracle_compare(S, p, comp, np64(t["K"]), np64(t["V"]), np64(t["Qwin"]), 0, TOL[w.dtype])
+    record("gqa_union_full_size", "ctx100k layer 0", **counts)
+
+
 # ------------------------------------------------------------------ RoPE repositioning (Eq. 7)
 ROPE = [
     dict(batch=1, H=2, d=64, n=512, dtype="fp32", theta=10000.0),
