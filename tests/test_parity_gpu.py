@@ -1096,6 +1096,23 @@ def _oracle_mode_compare(S, p, comp, case, K64, V64, Q64, tag):
             record(tag, f"{case} b{b} h{h}", **counts)
 
 
+@pytest.mark.parametrize("mode", [dict(route_mode="bucket_nearest"), dict(merge_keys=1)],
+                         ids=["bucket_nearest", "merge_keys"])
+def test_alternative_modes_full_size(S, mode):
+    """The nearest-kept fallback and the merged-keys reading at the bench's
+    layer size (one ctx100k layer, 8 KV heads x 102400 tokens): the whole
+    GPU pipeline, then KV heads 0 and 1 against the oracle's pipeline in the
+    same mode (near-ties of selection and routing counted)."""
+    w = synth.WORKLOADS["ctx100k"]
+    t = synth.make_layer(w, 0, DEV)
+    p = make_params(S, case_from_workload(w), **mode)
+    comp = S.Compressor(p, DEV).run(t["K"], t["V"], t["Qwin"])
+    torch.cuda.synchronize()
+    case = dict(batch=1, H=2, G=w.group, d=w.head_dim, n=w.seq_len, W=w.window, dtype=w.dtype)
+    _oracle_mode_compare(S, p, comp, case, np64(t["K"][:, :2]), np64(t["V"][:, :2]), np64(t["Qwin"][:, :2 * w.group]),
+                         "alternative_modes_full_size_" + ("bucket_nearest" if "route_mode" in mode else "merge_keys"))
+
+
 @pytest.mark.parametrize("case", READINGS + [dict(c, route_mode="coattn") for c in COATTN],
                          ids=[f"reading{i}" for i in range(len(READINGS))] + [f"coattn{i}" for i in range(len(COATTN))])
 def test_alternative_modes_end_to_end(S, case):
