@@ -733,7 +733,7 @@ def test_rope_reposition(S, case):
 
 
 # ------------------------------------------------------------------ generation loop with appended tokens
-@pytest.mark.parametrize("name", ["tiny", "llama_layer"])
+@pytest.mark.parametrize("name", ["tiny", "llama_layer", "ctx100k"])
 def test_decode_with_appended_tokens(S, name):
     """The decode loop after compression: each step appends the new token's
     key and value (bias 0) to the compressed cache and attends over all of
