@@ -214,14 +214,16 @@ MAX_SHAPES = [
     (dict(batch=1, H=1, G=8, d=64, n=1024, W=512, dtype="bf16"), None),
     # the most heads a call may take (batch * H = 65535, the grid's y limit); three heads sampled
     (dict(batch=65535, H=1, G=1, d=64, n=48, W=8, dtype="fp32"), [(0, 0), (32767, 0), (65534, 0)]),
+    # a long sequence: 2^20 tokens in one head (the ABI takes up to 2^28), 262144 kept
+    (dict(batch=1, H=1, G=2, d=64, n=1 << 20, W=32, dtype="bf16"), None),
 ]
 
 
-@pytest.mark.parametrize("case,heads", MAX_SHAPES, ids=["max_window_rows", "max_heads"])
+@pytest.mark.parametrize("case,heads", MAX_SHAPES, ids=["max_window_rows", "max_heads", "long_sequence"])
 def test_maximum_shapes_stagewise(S, case, heads):
-    """The largest shapes the ABI accepts along its two capped axes, every
-    stage checked against the oracle (on sampled heads for the head cap), plus
-    one decode step."""
+    """The largest shapes the ABI accepts along its two capped axes, and a
+    sequence of 2^20 tokens, every stage checked against the oracle (on
+    sampled heads for the head cap), plus one decode step."""
     t = synth.random_case(case["n"] * 3 + case["G"], batch=case["batch"], n_heads_kv=case["H"], group=case["G"],
                           head_dim=case["d"], seq_len=case["n"], window=case["W"], dtype=case["dtype"], device=DEV)
     p = make_params(S, case)
